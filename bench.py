@@ -1,0 +1,180 @@
+"""Benchmark of one draft-verify round on one MI355X.
+
+A step is the whole round on resident inputs, on one stream:
+  sv_alloc_budget (D-cut: prefix scores, global top-K, cost-table ratio, packing)
+  sv_verify_attn  (one layer of verify attention over the paged KV cache)
+  sv_spec_accept  (softmax of bf16 logits, accept test, first-reject cut, residual/bonus draw)
+Workload (default): concurrency 64, block 16 (15 drafts + the certain token), bf16,
+64 query / 8 KV heads of dim 128, committed context lognormal (median 4096, clipped
+to [512, 32768]) in 64-token pages, vocabulary 131072, per-request draft noise drawn
+from {0.3, 1.0, 2.0}, budget ratio chosen by a linear-plus-step cost table.
+
+Metric: verified draft tokens per second (sum of kept drafts n_i per step / step time).
+One JSON line on stdout; progress on stderr.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def attn_bytes(cfg, L, k):
+    """Algorithmic HBM bytes of one verify-attention call: every visible K and V row
+    read once per kv-head, plus q read and out written once."""
+    import numpy as np
+    e = 4 if cfg.dtype == "f32" else 2
+    kv = float(np.sum(L + k)) * 2 * cfg.Hkv * cfg.d * e
+    qo = float(np.sum(k)) * cfg.Hq * cfg.d * e * 2
+    return kv + qo
+
+
+def accept_bytes(cfg, k):
+    """Algorithmic bytes of acceptance: each kept target row (n_i+1 per request) and
+    each tested draft row (n_i) read once."""
+    import numpy as np
+    e = 4 if cfg.dtype == "f32" else 2
+    n = k - 1
+    return float(np.sum((n + 1) + n)) * cfg.V * e
+
+
+def cpu_baseline(cfg, rnd, n_req):
+    """The oracle, as it stands, on the first n_req requests of the same round."""
+    import numpy as np
+    import oracle
+    from paper_2607_25852_amd import synth
+    qo = rnd.qo_host
+    sub = np.arange(n_req)
+    k = np.diff(qo)[sub]
+    qo_s = synth.indptr_from_depths(k)
+    t0 = time.perf_counter()
+    # budget over the whole batch (the selection is global)
+    oracle.budget(rnd.lr["conf"], "cost", cost=synth.profiled_cost(cfg.R, cfg.b))
+    # attention for the sampled requests (every row and head)
+    kv = rnd.kv
+    pt = kv["page_table"][sub]
+    q = synth.pack_rows(kv["q_full"][sub], qo_s)
+    oracle.attention(q, kv["k_cache"], kv["v_cache"], pt, qo_s, rnd.kv_lens_host[sub], dtype=cfg.dtype)
+    # acceptance for the sampled requests
+    target = synth.pack_rows(rnd.lr["target_full"][sub], qo_s)
+    oracle.accept(target, rnd.lr["draft"][sub], rnd.lr["draft_tokens"][sub], qo_s, rnd.ua_host[sub],
+                  rnd.us_host[sub], kind="logits", dtype=cfg.dtype)
+    dt = time.perf_counter() - t0
+    drafts = float(np.sum(k - 1))
+    return dict(value=drafts / dt, unit="verified draft tokens/s", cores=oracle.num_threads(), kind="oracle",
+                sample=f"budget over all {cfg.R} requests + attention and acceptance of requests 0..{n_req - 1} "
+                       f"({int(drafts)} kept drafts, {dt:.1f} s)")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c64_b16")
+    ap.add_argument("--kv-split", type=int, default=0)
+    ap.add_argument("--cpu-requests", type=int, default=4, help="requests in the oracle sample (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the round's kernels run on a single MI355X and this build "
+              "has no multi-GPU path (see the sharding note in DESIGN.md); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2607_25852_amd import binding, synth
+    from paper_2607_25852_amd.round import DeviceRound
+
+    binding.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = synth.CONFIGS[args.workload]
+    log("generating inputs", cfg.name)
+    t0 = time.perf_counter()
+    rnd = DeviceRound(cfg, kind="logits", kv_split=args.kv_split)
+    torch.cuda.synchronize()
+    log(f"inputs resident ({time.perf_counter() - t0:.1f} s); K={rnd.K}")
+    k = np.diff(rnd.qo_host)
+    drafts = int(np.sum(k - 1))
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        rnd.run()
+    torch.cuda.synchronize()
+    # the selection is deterministic: the timed steps see the same qo_indptr
+    assert np.array_equal(rnd.qo.cpu().numpy(), rnd.qo_host)
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for s in range(args.steps):
+        e = ev[s]
+        e[0].record(stream)
+        rnd.run_budget()
+        e[1].record(stream)
+        rnd.run_attn()
+        e[2].record(stream)
+        rnd.run_accept()
+        e[3].record(stream)
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    ms_step = (t_end - t_start) * 1e3 / args.steps
+    t_budget = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    t_attn = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    t_acc = float(np.mean([e[2].elapsed_time(e[3]) for e in ev]))
+    value = drafts / (ms_step * 1e-3)
+    a_bytes = attn_bytes(cfg, rnd.L, k)
+    x_bytes = accept_bytes(cfg, k)
+    a_gbs = a_bytes / (t_attn * 1e-3) / 1e9
+    x_gbs = x_bytes / (t_acc * 1e-3) / 1e9
+    log(f"step {ms_step:.3f} ms: budget {t_budget * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us "
+        f"({a_gbs:.0f} GB/s), acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
+
+    cpu = None
+    if args.cpu_requests > 0:
+        log("timing the oracle on the host")
+        cpu = cpu_baseline(cfg, rnd, min(args.cpu_requests, cfg.R))
+
+    res = {
+        "metric": "verified draft tokens/sec/GPU",
+        "value": value,
+        "unit": "verified draft tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: concurrency {cfg.R}, block {cfg.b}, Hq {cfg.Hq}/Hkv {cfg.Hkv}/d {cfg.d}, "
+                               f"lognormal context median 4096 in [512, 32768], page {cfg.page}, vocab {cfg.V}, "
+                               f"cost-table budget",
+                   "concurrency": cfg.R, "block": cfg.b, "verified_positions": int(rnd.K),
+                   "verified_drafts": drafts, "budget_ratio_index": int(rnd.sel[1].item()),
+                   "parallelism": "single GPU"},
+        "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (split-KV attention + partial merge)",
+                     "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes": a_bytes},
+        "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
+                    "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
+                    "acceptance_algorithmic_bytes": x_bytes},
+        "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,216 @@
+/*
+ * specverify.h -- C ABI of libspecverify: the data-parallel core of one
+ * speculative-decoding draft-verify round on an AMD Instinct MI355X (gfx950).
+ *
+ * The round (AngelSpec, Sec. 4 "Real-World Deployment: D-cut", and the
+ * rejection-sampling verification of Sec. 1) has three steps, one call each:
+ *
+ *   sv_alloc_budget  D-cut verification budget: prefix confidence scores, a
+ *                    global top-K over every request's draft positions, the
+ *                    budget ratio chosen against a profiled cost, and the dense
+ *                    packing of the kept positions (qo_indptr).
+ *   sv_verify_attn   attention of every kept position over its request's paged
+ *                    KV cache: causal inside the block, full over the context,
+ *                    grouped-query heads.
+ *   sv_spec_accept   speculative acceptance: softmax of the target logits, the
+ *                    per-position test u < min(1, p/q), the first-rejection
+ *                    cut, and the extra token drawn from the normalised residual
+ *                    max(p - q, 0), or from p when the whole block survives.
+ *
+ * Conventions shared by every entry point
+ *   - All array pointers are caller-owned DEVICE memory unless marked "host".
+ *     The library allocates nothing and keeps no state between calls; each call
+ *     only enqueues kernels on `stream` (a hipStream_t; NULL = the default
+ *     stream) and returns without waiting for them.
+ *   - Descriptors are host structs, read during the call only.
+ *   - Host-side argument checks run before anything is enqueued. On failure the
+ *     call returns a non-zero sv_status, enqueues nothing, and sv_last_error()
+ *     (thread-local) describes the reason. A failed launch returns SV_ERR_HIP.
+ *   - Device data is not validated beyond what keeps every memory access in
+ *     bounds (page ids, row ranges and token ids are range-checked by the
+ *     kernels); out-of-range values give unspecified but finite-memory results.
+ *   - "b" (block) is the number of verify positions per request: the certain
+ *     token that ends the committed context plus D = b - 1 draft tokens.
+ *     Position 0 is the certain token; drafts are positions 1..D.
+ *   - Uniform random numbers are inputs (the caller's generator), fp32 in [0,1).
+ *   - Calls on different streams may run concurrently (no shared state); calls
+ *     sharing a workspace buffer must be ordered by the caller.
+ */
+#ifndef SPECVERIFY_H
+#define SPECVERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SV_ABI_VERSION 1
+
+typedef enum {
+    SV_OK = 0,
+    SV_ERR_INVALID_ARG = 1, /* a descriptor field or pointer is invalid */
+    SV_ERR_UNSUPPORTED = 2, /* valid request outside what the kernels implement */
+    SV_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the size query */
+    SV_ERR_HIP = 4          /* a HIP launch failed (see sv_last_error) */
+} sv_status;
+
+typedef enum { SV_F32 = 0, SV_BF16 = 1 } sv_dtype;
+typedef enum { SV_LOGITS = 0, SV_PROBS = 1 } sv_input_kind;
+typedef enum { SV_BUDGET_FIXED = 0, SV_BUDGET_COST = 1 } sv_budget_mode;
+
+#define SV_MAX_BLOCK 16            /* b <= 16 verify positions per request */
+#define SV_MAX_RATIOS 8
+#define SV_MAX_BUDGET_REQS 4096    /* R for sv_alloc_budget */
+#define SV_MAX_BUDGET_POSITIONS 8192 /* R * b for sv_alloc_budget */
+#define SV_MAX_VOCAB (1 << 22)
+
+/* ------------------------------------------------------------------------- */
+/* D-cut budget (Sec. 4.2, eqs. dcut-score, dcut-expected-advance,            */
+/* dcut-budget, dcut-batch-utility, dcut-select, and "Packing and correctness")*/
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_reqs;     /* R >= 1 (the paper's B, active requests)            */
+    int32_t block;        /* b in [1, 16]                                        */
+    int32_t mode;         /* sv_budget_mode                                       */
+    int32_t fixed_budget; /* FIXED: K with R <= K <= R*b                          */
+    int32_t num_ratios;   /* COST: 1..8 candidate ratios                          */
+    int32_t ratio_permille[SV_MAX_RATIOS]; /* COST: strictly ascending, (0, 1000] */
+    uint32_t cost[SV_MAX_RATIOS]; /* COST: profiled step cost C(R, rho_j) > 0,
+                                     any integer time unit                      */
+} sv_budget_desc;
+
+/*
+ * sv_alloc_budget -- choose how many draft positions of each request to verify.
+ *
+ *   scores   s[i][0] = 1, s[i][t] = s[i][t-1] * c[i][t], an fp32 product taken
+ *            left to right (eq. dcut-score); a confidence is clamped to [0,1]
+ *            first and NaN counts as 0, which keeps scores non-increasing.
+ *   order    all R*b positions ranked by score (higher first), ties to the
+ *            shallower position (Sec. 4.2), then to the lower request index;
+ *            taking the first K in this order keeps a contiguous prefix of
+ *            every request's block.
+ *   budget   FIXED: K = fixed_budget.  COST: for each ratio rho_j,
+ *            K_j = max(R, ceil(rho_j * R * b)) (eq. dcut-budget); utility
+ *            U_j = sum of the top-K_j scores, each as floor(s * 2^40) in
+ *            uint64 (eq. dcut-batch-utility, in fixed point); the chosen ratio
+ *            maximises U_j / C_j, compared exactly as U_a*C_b vs U_b*C_a in
+ *            128 bits, ties to the smaller ratio (eq. dcut-select).
+ *   packing  n_i = kept positions of request i minus 1 (drafts kept),
+ *            qo_indptr = exclusive prefix sum of n_i + 1: the rows of request i
+ *            in the dense verify batch are qo_indptr[i] .. qo_indptr[i+1]-1.
+ *
+ * conf       [R, b-1] fp32, c[i][t] for drafts t = 1..b-1 (may be NULL if b = 1)
+ * keep       [R] int32 out: n_i in [0, b-1]
+ * qo_indptr  [R+1] int32 out
+ * sel        [2] int32 out: {K, index of the chosen ratio or -1 in FIXED mode}
+ * scores     [R, b] fp32 out, or NULL
+ * utility    [num_ratios] uint64 out (COST) or [1] (FIXED: U of the fixed K), or NULL
+ * Limits: R <= 4096, R*b <= 8192. One workgroup; no workspace.
+ */
+sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t* keep,
+                          int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
+                          void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Verify attention (every kept position is evaluated by the target model,    */
+/* Sec. 4.1; the dense packed batch of Sec. 4.2).                             */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_reqs;          /* R >= 1                                            */
+    int32_t total_q_max;       /* rows allocated in q / out / lse (>= qo_indptr[R])  */
+    int32_t block;             /* max k_i (<= 16)                                   */
+    int32_t num_q_heads;       /* Hq                                               */
+    int32_t num_kv_heads;      /* Hkv, Hq % Hkv == 0; G = Hq / Hkv                   */
+    int32_t head_dim;          /* d: bf16 64 or 128; fp32 any multiple of 4 <= 256  */
+    int32_t page_size;         /* P tokens per page, a power of two in [1, 4096]    */
+    int32_t max_pages_per_req; /* columns of page_table                              */
+    int32_t num_pages;         /* pages in each cache                                */
+    int32_t max_kv_len;        /* upper bound of kv_lens[i]                           */
+    int32_t dtype;             /* sv_dtype of q, caches and out                       */
+    float sm_scale;            /* logit scale; 0 means 1/sqrt(d)                      */
+    int32_t kv_split;          /* tokens per split-KV work item (multiple of 64), 0 = auto */
+} sv_attn_desc;
+
+/*
+ * sv_verify_attn -- for request i with k_i = qo_indptr[i+1]-qo_indptr[i] rows
+ * and committed context L_i = kv_lens[i] - k_i, query row j (0 <= j < k_i) of
+ * head h attends to keys s = 0 .. L_i + j of kv-head floor(h / G):
+ *     z_s = sm_scale * <q, K_s>,  lse = ln sum_s exp(z_s),  o = sum_s exp(z_s - lse) V_s.
+ * Key s of request i sits in page page_table[i][s / P], slot s % P. The block's
+ * own keys and values (positions L_i .. L_i + k_i - 1) must already be in the
+ * cache; pages and slots past kv_lens[i] are never read.
+ *
+ * q          [total_q_max, Hq, d]  (rows packed by qo_indptr)
+ * k_cache, v_cache [num_pages, Hkv, P, d]
+ * page_table [R, max_pages_per_req] int32
+ * qo_indptr  [R+1] int32 (1 <= k_i <= block), kv_lens [R] int32 (k_i <= kv_lens[i] <= max_kv_len)
+ * out        [total_q_max, Hq, d] same dtype as q;  lse [total_q_max, Hq] fp32 or NULL
+ * ws         scratch of at least sv_verify_attn_workspace_size(desc) bytes
+ *            (partial results of split-KV work items), device memory.
+ * bf16 runs on MFMA with fp32 accumulation; fp32 runs on vector ALUs in fp32.
+ */
+sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
+                         const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes,
+                         void* stream);
+size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc);
+
+/* ------------------------------------------------------------------------- */
+/* Speculative acceptance (rejection-sampling verification, Sec. 1; the       */
+/* acceptance probability of eq. mtp-acceptance-tv)                           */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_reqs;   /* R >= 1                                            */
+    int32_t block;      /* b in [1, 16]                                        */
+    int32_t vocab;      /* V in [1, 2^22]                                      */
+    int32_t kind;       /* sv_input_kind: LOGITS (fp32 or bf16) or PROBS (fp32) */
+    int32_t dtype;      /* sv_dtype of target and draft                         */
+    float temperature;  /* LOGITS: p = softmax(logits / T), T > 0               */
+} sv_accept_desc;
+
+/*
+ * sv_spec_accept -- for request i with n_i = qo_indptr[i+1]-qo_indptr[i]-1 drafts:
+ *   P_r = target row qo_indptr[i]+r (r = 0..n_i): the target distribution of
+ *         block position r+1;  Q_t = draft row (i, t-1): the draft distribution
+ *         of draft t (t = 1..n_i), d_t = draft_tokens[i][t-1].
+ *   1. draft t is accepted iff u_accept[i][t-1] * Q_t(d_t) < P_{t-1}(d_t),
+ *      evaluated exactly (fp64 product of fp32 values);
+ *   2. a_i = (first rejected t) - 1, or n_i when none is rejected;
+ *   3. extra token: after a rejection from r = max(P_{a_i} - Q_{a_i+1}, 0)
+ *      (fp32 difference), else from r = P_{n_i}; drawn by the inverse CDF of the
+ *      integer weights w(v) = floor(min(r(v),1) * 2^40): the smallest v whose
+ *      running sum of w exceeds floor(m * Z / 2^24), m = floor(u_sample[i] * 2^24),
+ *      Z = sum w. An empty residual (Z = 0) falls back to P_{a_i} (flag bit 0);
+ *      if that is empty too the token is -1 (flag bit 1);
+ *   4. out_tokens[i] = d_1 .. d_{a_i}, token, then -1; accept_len[i] = a_i.
+ *   A draft token outside [0, V) is rejected (flag bit 2).
+ * In LOGITS mode the probabilities are softmax(logits / T) computed in fp32 on
+ * the GPU (row max and sum of exponentials per row, read once).
+ *
+ * target      [qo_indptr[R], V] rows packed by qo_indptr (fp32 or bf16)
+ * draft       [R, b-1, V] (fp32 or bf16); only rows t-1 < n_i are read
+ * draft_tokens, u_accept [R, b-1] (int32, fp32); u_sample [R] fp32
+ * qo_indptr   [R+1] int32 with 0 <= n_i <= b-1
+ * accept_len  [R] int32 out; out_tokens [R, b] int32 out; flags [R] int32 out or NULL
+ * ws          scratch of at least sv_spec_accept_workspace_size(desc) bytes.
+ */
+sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const void* draft,
+                         const int32_t* draft_tokens, const int32_t* qo_indptr,
+                         const float* u_accept, const float* u_sample, int32_t* accept_len,
+                         int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
+                         void* stream);
+size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc);
+
+/* ------------------------------------------------------------------------- */
+/* status                                                                      */
+/* ------------------------------------------------------------------------- */
+const char* sv_status_string(int32_t status); /* static string, never NULL        */
+const char* sv_last_error(void);              /* thread-local, "" when none        */
+int32_t sv_abi_version(void);                 /* SV_ABI_VERSION                    */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECVERIFY_H */

@@ -105,7 +105,7 @@ def accept(target, draft, draft_tokens, qo_indptr, u_accept, u_sample, kind="pro
     draft [R, b-1, V]; draft_tokens [R, b-1] int32; qo_indptr [R+1];
     u_accept [R, b-1] fp32; u_sample [R] fp32.
     Returns dict(accept_len [R], out_tokens [R, b], flags [R]) and, with
-    diagnostics, p_at/q_at [R, b-1] and cdf [R, 3] = (thr, cum before token, Z).
+    diagnostics, p_at/q_at [R, b-1] and cdf [R, 4] = (thr, cum before token, token weight, Z).
     """
     dt = 0 if dtype == "f32" else 1
     knd = 1 if kind == "probs" else 0
@@ -123,7 +123,7 @@ def accept(target, draft, draft_tokens, qo_indptr, u_accept, u_sample, kind="pro
     flags = np.empty(R, np.int32)
     dp = np.zeros((R, D), np.float64) if diagnostics else None
     dq = np.zeros((R, D), np.float64) if diagnostics else None
-    dc = np.zeros((R, 3), np.float64) if diagnostics else None
+    dc = np.zeros((R, 4), np.float64) if diagnostics else None
     rc = _load().oracle_accept(R, b, V, knd, dt, float(temperature), _ptr(target), _ptr(draft),
                                _ptr(dtok), _ptr(qo), _ptr(ua), _ptr(us), _ptr(acc), _ptr(out),
                                _ptr(flags), _ptr(dp), _ptr(dq), _ptr(dc))

@@ -258,8 +258,8 @@ static float prow_prob(const prow_t* pr, int v) {
  * kind 0 = logits (p = softmax(l / T), fp64 internally, rounded to fp32),
  * kind 1 = probabilities given as fp32 rows.  dtype 0 = fp32, 1 = bf16 (logits only).
  * diag_p/diag_q [R, b-1] (nullable): P_{t-1}(d_t) and Q_t(d_t) as used by the test.
- * diag_cdf [R, 3] (nullable): (thr, cumulative weight before the token, Z) as doubles,
- * so a caller can see how far the draw is from a CDF step.
+ * diag_cdf [R, 4] (nullable): (thr, cumulative weight before the token, the token's
+ * weight, Z) as doubles, so a caller can see how far the draw is from a CDF step.
  */
 int oracle_accept(int R, int b, int V, int kind, int dtype, float temperature, const void* target,
                   const void* draft, const int* draft_tokens, const int* qo_indptr,
@@ -337,7 +337,7 @@ int oracle_accept(int R, int b, int V, int kind, int dtype, float temperature, c
             }
         }
         int token = -1;
-        double c_before = 0.0, thr_d = 0.0;
+        double c_before = 0.0, thr_d = 0.0, w_tok = 0.0;
         if (Z == 0) {
             flag |= 2;
         } else {
@@ -357,11 +357,13 @@ int oracle_accept(int R, int b, int V, int kind, int dtype, float temperature, c
             }
             c_before = (double)cum;
             thr_d = (double)thr;
+            if (token >= 0) w_tok = (double)w[token];
         }
         if (diag_cdf) {
-            diag_cdf[(int64_t)i * 3 + 0] = thr_d;
-            diag_cdf[(int64_t)i * 3 + 1] = c_before;
-            diag_cdf[(int64_t)i * 3 + 2] = (double)Z;
+            diag_cdf[(int64_t)i * 4 + 0] = thr_d;
+            diag_cdf[(int64_t)i * 4 + 1] = c_before;
+            diag_cdf[(int64_t)i * 4 + 2] = w_tok;
+            diag_cdf[(int64_t)i * 4 + 3] = (double)Z;
         }
         free(w);
         /* step 4: commit */

@@ -1,0 +1,484 @@
+// Speculative acceptance (rejection-sampling verification, AngelSpec Sec. 1; per-position
+// acceptance probability min(1, p/q) whose expectation is the overlap of eq.
+// mtp-acceptance-tv).
+//
+// Four kernels on one stream:
+//   rowstats  (logits mode only) streams every needed row once -- the n_i+1 target rows
+//             and n_i draft rows of each request -- and writes per-chunk (max, sum of
+//             exponentials). This is the HBM-bound pass.
+//   decide    one wavefront per request: merges the chunk statistics, evaluates the
+//             acceptance test of every draft in its own lane (exact fp64 product
+//             u*q < p), finds the first rejection with a ballot, writes the accepted
+//             prefix and the plan of the extra-token draw.
+//   ressum    per (request, vocabulary chunk): integer weights floor(r * 2^40) of the
+//             residual max(p - q, 0) (or of p for the bonus) and their chunk sums.
+//   search    per request: Z = sum of chunk sums, threshold floor(m * Z / 2^24), the
+//             chunk holding it, then the exact token inside that chunk.
+// Every sum that decides a token is an integer sum, so the result does not depend on
+// how the vocabulary is split across threads.
+#include "sv_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace sv {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kThreads = 256;
+constexpr int kStatsLoads = 8;  // 16-byte loads in flight per thread in rowstats
+
+struct ReqPlan {
+    int a, n, mode, flag;  // mode 0: residual after a rejection, 1: bonus, 2: nothing to draw
+    int rowP, rowQ;        // target row of P_a (or P_n), draft row of Q_{a+1}
+    float mP, iSP, mQ, iSQ;
+};
+
+struct AcceptArgs {
+    const void* target;
+    const void* draft;
+    const int32_t* tokens;
+    const int32_t* qo;
+    const float* ua;
+    const float* us;
+    int32_t* accept_len;
+    int32_t* out_tokens;
+    int32_t* flags;
+    float2* stats_t;  // [R*b][NC]
+    float2* stats_q;  // [R*D][NC]
+    ReqPlan* plan;    // [R]
+    uint64_t* csum;   // [R][NCR][2]
+    int R, b, D, V, NC, stats_chunk, NCR, res_chunk;
+    float invT;
+};
+
+__device__ inline float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+__device__ inline float to_f(float x) { return x; }
+__device__ inline float to_f(uint16_t h) { return bf2f(h); }
+
+template <typename T>
+__device__ inline float load_x(const T* row, int v) { return to_f(row[v]); }
+
+// fp32 probability of token v of a row: softmax(l / T) from its (max, 1/sum) in logits
+// mode, the stored value in probability mode. Every kernel uses this one function.
+template <bool LOGITS, typename T>
+__device__ inline float prob_of(const T* row, int v, float m, float iS, float invT) {
+    if (LOGITS) {
+        const float x = load_x<T>(row, v) * invT;
+        return __builtin_amdgcn_exp2f((x - m) * kLog2e) * iS;
+    } else {
+        return load_x<T>(row, v);
+    }
+}
+
+__device__ inline uint64_t weight_of(float r) {
+    if (!(r > 0.0f)) return 0;
+    if (r > 1.0f) r = 1.0f;
+    return (uint64_t)(r * 1099511627776.0f);  // exact: power-of-two scaling
+}
+
+template <typename T>
+__device__ inline const T* row_ptr(const void* base, long long row, int V) {
+    return (const T*)base + row * (long long)V;
+}
+
+// ----------------------------------------------------------------------------------
+// rowstats: grid (NC, R*b + R*D)
+// ----------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
+    constexpr int VEC = 16 / sizeof(T);
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+    __shared__ float red[kThreads / 64];
+
+    const int slot = blockIdx.y;
+    const int RB = a.R * a.b;
+    const T* row;
+    float2* dst;
+    if (slot < RB) {
+        const int K = a.qo[a.R];
+        if (slot >= K) return;
+        row = row_ptr<T>(a.target, slot, a.V);
+        dst = a.stats_t + (size_t)slot * a.NC;
+    } else {
+        const int s2 = slot - RB;
+        const int i = s2 / a.D, t = s2 % a.D;
+        const int n = a.qo[i + 1] - a.qo[i] - 1;
+        if (t >= n) return;
+        row = row_ptr<T>(a.draft, (long long)i * a.D + t, a.V);
+        dst = a.stats_q + (size_t)(i * a.D + t) * a.NC;
+    }
+    const int c = blockIdx.x;
+    const int beg = c * a.stats_chunk;
+    const int end = min(a.V, beg + a.stats_chunk);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+
+    float x[kStatsLoads * VEC];
+    const bool vec_ok = (a.V % VEC) == 0 && (end - beg) == a.stats_chunk;
+    if (vec_ok) {
+        const vec_t* rv = (const vec_t*)(row + beg);
+#pragma unroll
+        for (int k = 0; k < kStatsLoads; k++) {
+            const vec_t v = rv[tid + k * kThreads];
+#pragma unroll
+            for (int e = 0; e < VEC; e++) x[k * VEC + e] = to_f(v[e]) * a.invT;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < kStatsLoads; k++)
+#pragma unroll
+            for (int e = 0; e < VEC; e++) {
+                const int v = beg + (tid + k * kThreads) * VEC + e;
+                x[k * VEC + e] = v < end ? load_x<T>(row, v) * a.invT : -INFINITY;
+            }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < kStatsLoads * VEC; e++) mx = fmaxf(mx, x[e]);
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    if (lane == 0) red[w] = mx;
+    __syncthreads();
+    mx = red[0];
+#pragma unroll
+    for (int k = 1; k < kThreads / 64; k++) mx = fmaxf(mx, red[k]);
+    __syncthreads();
+    float s = 0.0f;
+    if (mx != -INFINITY) {
+#pragma unroll
+        for (int e = 0; e < kStatsLoads * VEC; e++) s += __builtin_amdgcn_exp2f((x[e] - mx) * kLog2e);
+    }
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane == 0) red[w] = s;
+    __syncthreads();
+    if (tid == 0) {
+        float tot = 0.0f;
+        for (int k = 0; k < kThreads / 64; k++) tot += red[k];
+        dst[c] = make_float2(mx, tot);
+    }
+}
+
+__device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS) {
+    float mm = -INFINITY;
+    for (int c = 0; c < NC; c++) mm = fmaxf(mm, st[c].x);
+    float S = 0.0f;
+    if (mm != -INFINITY)
+        for (int c = 0; c < NC; c++)
+            if (st[c].x != -INFINITY) S += st[c].y * __builtin_amdgcn_exp2f((st[c].x - mm) * kLog2e);
+    m = mm;
+    iS = S > 0.0f ? 1.0f / S : 0.0f;
+}
+
+// ----------------------------------------------------------------------------------
+// decide: one wavefront per request
+// ----------------------------------------------------------------------------------
+template <bool LOGITS, typename T>
+__global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
+    const int i = blockIdx.x, lane = threadIdx.x;
+    const int q0 = a.qo[i];
+    const int n = a.qo[i + 1] - q0 - 1;
+    const int K = a.qo[a.R];
+    ReqPlan pl{};
+    if (n < 0 || n > a.D || q0 < 0 || q0 + n + 1 > K || K > a.R * a.b) {  // malformed packing: nothing to draw
+        if (lane == 0) {
+            pl.mode = 2;
+            pl.flag = 2;
+            a.plan[i] = pl;
+            a.accept_len[i] = 0;
+        }
+        for (int t = lane; t < a.b; t += 64) a.out_tokens[(size_t)i * a.b + t] = -1;
+        return;
+    }
+    // per-row softmax statistics: lane r -> P_r (r <= n), lane 32+t -> Q_{t+1} (t < n)
+    float m = 0.0f, iS = 0.0f;
+    if (LOGITS) {
+        if (lane <= n) merge_stats(a.stats_t + (size_t)(q0 + lane) * a.NC, a.NC, m, iS);
+        else if (lane >= 32 && lane - 32 < n) merge_stats(a.stats_q + (size_t)(i * a.D + lane - 32) * a.NC, a.NC, m, iS);
+    }
+    // the test of draft t+1 in lane t: P_t(d) vs u * Q_{t+1}(d)
+    const float mPt = __shfl(m, lane & 31, 64), iSPt = __shfl(iS, lane & 31, 64);
+    const float mQt = __shfl(m, 32 + (lane & 31), 64), iSQt = __shfl(iS, 32 + (lane & 31), 64);
+    bool reject = false, bad_tok = false;
+    int d = -1;
+    if (lane < n) {
+        d = a.tokens[(size_t)i * a.D + lane];
+        if (d < 0 || d >= a.V) {
+            reject = true;
+            bad_tok = true;
+        } else {
+            const float p = prob_of<LOGITS, T>(row_ptr<T>(a.target, q0 + lane, a.V), d, mPt, iSPt, a.invT);
+            const float q = prob_of<LOGITS, T>(row_ptr<T>(a.draft, (long long)i * a.D + lane, a.V), d, mQt, iSQt, a.invT);
+            const double u = (double)a.ua[(size_t)i * a.D + lane];
+            reject = !(u * (double)q < (double)p);
+        }
+    }
+    const uint64_t fails = __ballot(reject);
+    const int acc = fails ? __builtin_ctzll(fails) : n;
+    const int badflag = __shfl((int)bad_tok, acc & 63, 64) ? 4 : 0;
+    for (int t = lane; t < a.b; t += 64) {
+        if (t < acc) a.out_tokens[(size_t)i * a.b + t] = a.tokens[(size_t)i * a.D + t];
+        else if (t > acc) a.out_tokens[(size_t)i * a.b + t] = -1;
+    }
+    // statistics of P_a (lane a) and Q_{a+1} (lane 32+a), gathered by every lane
+    const float pm = __shfl(m, acc & 31, 64), piS = __shfl(iS, acc & 31, 64);
+    const float qm = __shfl(m, 32 + (acc & 31), 64), qiS = __shfl(iS, 32 + (acc & 31), 64);
+    if (lane == 0) {
+        pl.a = acc;
+        pl.n = n;
+        pl.flag = acc < n ? badflag : 0;
+        pl.mode = acc < n ? 0 : 1;
+        pl.rowP = q0 + acc;
+        pl.rowQ = acc < n ? i * a.D + acc : -1;
+        pl.mP = pm;
+        pl.iSP = piS;
+        pl.mQ = acc < n ? qm : 0.0f;
+        pl.iSQ = acc < n ? qiS : 0.0f;
+        a.plan[i] = pl;
+        a.accept_len[i] = acc;
+    }
+}
+
+// weights of token v for a plan: (w_res, w_p) -- w_res is the residual (or bonus) weight,
+// w_p the fallback weight of P_a used when the residual is empty
+template <bool LOGITS, typename T>
+__device__ inline void weights_at(const AcceptArgs& a, const ReqPlan& pl, int v, uint64_t& wr, uint64_t& wp) {
+    const float pv = prob_of<LOGITS, T>(row_ptr<T>(a.target, pl.rowP, a.V), v, pl.mP, pl.iSP, a.invT);
+    if (pl.mode == 0) {
+        const float qv = prob_of<LOGITS, T>(row_ptr<T>(a.draft, pl.rowQ, a.V), v, pl.mQ, pl.iSQ, a.invT);
+        float r = pv - qv;
+        if (!(r > 0.0f)) r = 0.0f;
+        wr = weight_of(r);
+        wp = weight_of(pv);
+    } else {
+        wr = weight_of(pv);
+        wp = 0;
+    }
+}
+
+__device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    __syncthreads();
+    if (lane == 0) red[w] = v;
+    __syncthreads();
+    uint64_t t = 0;
+    for (int k = 0; k < kThreads / 64; k++) t += red[k];
+    return t;
+}
+
+// ----------------------------------------------------------------------------------
+// ressum: grid (NCR, R)
+// ----------------------------------------------------------------------------------
+template <bool LOGITS, typename T>
+__global__ __launch_bounds__(kThreads) void ressum_kernel(AcceptArgs a) {
+    __shared__ uint64_t red[kThreads / 64];
+    const int i = blockIdx.y, c = blockIdx.x;
+    const ReqPlan pl = a.plan[i];
+    if (pl.mode == 2) return;
+    const int beg = c * a.res_chunk, end = min(a.V, beg + a.res_chunk);
+    uint64_t sr = 0, sp = 0;
+    for (int v = beg + threadIdx.x; v < end; v += kThreads) {
+        uint64_t wr, wp;
+        weights_at<LOGITS, T>(a, pl, v, wr, wp);
+        sr += wr;
+        sp += wp;
+    }
+    sr = block_sum_u64(sr, red);
+    sp = block_sum_u64(sp, red);
+    if (threadIdx.x == 0) {
+        a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
+        a.csum[((size_t)i * a.NCR + c) * 2 + 1] = sp;
+    }
+}
+
+// ----------------------------------------------------------------------------------
+// search: one workgroup per request
+// ----------------------------------------------------------------------------------
+template <bool LOGITS, typename T>
+__global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
+    __shared__ uint64_t red[kThreads / 64];
+    __shared__ uint64_t scan[kThreads];
+    __shared__ int s_chunk;
+    __shared__ uint64_t s_before;
+    __shared__ int s_token;
+    const int i = blockIdx.x, tid = threadIdx.x;
+    ReqPlan pl = a.plan[i];
+    if (pl.mode == 2) {
+        if (tid == 0 && a.flags) a.flags[i] = pl.flag;
+        return;
+    }
+    // Z of the residual and of the fallback
+    uint64_t zr = 0, zp = 0;
+    for (int c = tid; c < a.NCR; c += kThreads) {
+        zr += a.csum[((size_t)i * a.NCR + c) * 2 + 0];
+        zp += a.csum[((size_t)i * a.NCR + c) * 2 + 1];
+    }
+    zr = block_sum_u64(zr, red);
+    zp = block_sum_u64(zp, red);
+    int col = 0;
+    uint64_t Z = zr;
+    int flag = pl.flag;
+    if (Z == 0 && pl.mode == 0) {
+        col = 1;
+        Z = zp;
+        flag |= 1;
+    }
+    int token = -1;
+    if (Z == 0) {
+        flag |= 2;
+    } else {
+        const float u = a.us[i];
+        uint32_t mu;
+        if (!(u > 0.0f)) mu = 0;
+        else if (u >= 1.0f) mu = (1u << 24) - 1;
+        else mu = (uint32_t)(u * 16777216.0f);  // exact on the 2^-24 grid, truncates otherwise
+        const uint64_t thr = (uint64_t)(((unsigned __int128)mu * Z) >> 24);
+        // 1. chunk holding thr: scan of chunk sums in rounds of kThreads chunks
+        if (tid == 0) s_chunk = -1;
+        uint64_t base = 0;
+        for (int c0 = 0; c0 < a.NCR; c0 += kThreads) {
+            const int c = c0 + tid;
+            const uint64_t v = c < a.NCR ? a.csum[((size_t)i * a.NCR + c) * 2 + col] : 0;
+            scan[tid] = v;
+            __syncthreads();
+            for (int off = 1; off < kThreads; off <<= 1) {  // Hillis-Steele inclusive scan
+                const uint64_t add = tid >= off ? scan[tid - off] : 0;
+                __syncthreads();
+                scan[tid] += add;
+                __syncthreads();
+            }
+            const uint64_t incl = base + scan[tid];
+            const uint64_t excl = incl - v;
+            if (c < a.NCR && v > 0 && excl <= thr && thr < incl) {
+                s_chunk = c;
+                s_before = excl;
+            }
+            base += scan[kThreads - 1];
+            __syncthreads();
+            if (s_chunk >= 0) break;
+        }
+        const int c = s_chunk;
+        if (c >= 0) {
+            // 2. inside the chunk: contiguous per-thread ranges, exclusive scan, local search
+            const int beg = c * a.res_chunk, end = min(a.V, beg + a.res_chunk);
+            const int per = (a.res_chunk + kThreads - 1) / kThreads;
+            const int lo = beg + tid * per, hi = min(end, lo + per);
+            uint64_t loc = 0;
+            for (int v = lo; v < hi; v++) {
+                uint64_t wr, wp;
+                weights_at<LOGITS, T>(a, pl, v, wr, wp);
+                loc += col ? wp : wr;
+            }
+            scan[tid] = loc;
+            __syncthreads();
+            for (int off = 1; off < kThreads; off <<= 1) {
+                const uint64_t add = tid >= off ? scan[tid - off] : 0;
+                __syncthreads();
+                scan[tid] += add;
+                __syncthreads();
+            }
+            if (tid == 0) s_token = -1;
+            __syncthreads();
+            const uint64_t rel = thr - s_before;
+            const uint64_t excl = scan[tid] - loc;
+            if (loc > 0 && excl <= rel && rel < scan[tid]) {
+                uint64_t cum = s_before + excl;
+                for (int v = lo; v < hi; v++) {
+                    uint64_t wr, wp;
+                    weights_at<LOGITS, T>(a, pl, v, wr, wp);
+                    const uint64_t wv = col ? wp : wr;
+                    if (cum + wv > thr) {
+                        s_token = v;
+                        break;
+                    }
+                    cum += wv;
+                }
+            }
+            __syncthreads();
+            token = s_token;
+        }
+    }
+    if (tid == 0) {
+        a.out_tokens[(size_t)i * a.b + pl.a] = token;
+        if (a.flags) a.flags[i] = flag;
+    }
+}
+
+}  // namespace
+
+AcceptPlan plan_accept(const sv_accept_desc& d) {
+    AcceptPlan p{};
+    const int esz = d.dtype == SV_BF16 ? 2 : 4;
+    const int vec = 16 / esz;
+    p.stats_chunk = kThreads * kStatsLoads * vec;  // 32 KB of logits per workgroup
+    p.stats_chunks = (d.vocab + p.stats_chunk - 1) / p.stats_chunk;
+    p.res_chunk = 8192;
+    p.res_chunks = (d.vocab + p.res_chunk - 1) / p.res_chunk;
+    const size_t R = d.num_reqs, b = d.block, D = b > 1 ? b - 1 : 1;
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    size_t off = 0;
+    p.off_stats_t = off;
+    off = al(off + R * b * p.stats_chunks * sizeof(float2));
+    p.off_stats_q = off;
+    off = al(off + R * D * p.stats_chunks * sizeof(float2));
+    p.off_plan = off;
+    off = al(off + R * sizeof(ReqPlan));
+    p.off_csum = off;
+    off = al(off + R * p.res_chunks * 2 * sizeof(uint64_t));
+    p.total = off;
+    return p;
+}
+
+hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const void* target,
+                         const void* draft, const int32_t* draft_tokens, const int32_t* qo_indptr,
+                         const float* u_accept, const float* u_sample, int32_t* accept_len,
+                         int32_t* out_tokens, int32_t* flags, void* ws, hipStream_t stream) {
+    AcceptArgs a{};
+    a.target = target;
+    a.draft = draft;
+    a.tokens = draft_tokens;
+    a.qo = qo_indptr;
+    a.ua = u_accept;
+    a.us = u_sample;
+    a.accept_len = accept_len;
+    a.out_tokens = out_tokens;
+    a.flags = flags;
+    char* w = (char*)ws;
+    a.stats_t = (float2*)(w + p.off_stats_t);
+    a.stats_q = (float2*)(w + p.off_stats_q);
+    a.plan = (ReqPlan*)(w + p.off_plan);
+    a.csum = (uint64_t*)(w + p.off_csum);
+    a.R = d.num_reqs;
+    a.b = d.block;
+    a.D = d.block - 1;
+    a.V = d.vocab;
+    a.NC = p.stats_chunks;
+    a.stats_chunk = p.stats_chunk;
+    a.NCR = p.res_chunks;
+    a.res_chunk = p.res_chunk;
+    a.invT = d.kind == SV_LOGITS ? 1.0f / d.temperature : 1.0f;
+    const bool logits = d.kind == SV_LOGITS;
+    const bool bf = d.dtype == SV_BF16;
+    if (logits) {
+        const dim3 g(p.stats_chunks, d.num_reqs * d.block + d.num_reqs * (d.block > 1 ? d.block - 1 : 0));
+        if (bf) hipLaunchKernelGGL(rowstats_kernel<uint16_t>, g, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL(rowstats_kernel<float>, g, dim3(kThreads), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+#define SV_ACCEPT_PHASES(LG, TT)                                                                    \
+    hipLaunchKernelGGL((decide_kernel<LG, TT>), dim3(d.num_reqs), dim3(64), 0, stream, a);          \
+    hipLaunchKernelGGL((ressum_kernel<LG, TT>), dim3(p.res_chunks, d.num_reqs), dim3(kThreads), 0, \
+                       stream, a);                                                                  \
+    hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
+    if (logits && bf) {
+        SV_ACCEPT_PHASES(true, uint16_t);
+    } else if (logits) {
+        SV_ACCEPT_PHASES(true, float);
+    } else {
+        SV_ACCEPT_PHASES(false, float);
+    }
+#undef SV_ACCEPT_PHASES
+    return hipGetLastError();
+}
+
+}  // namespace sv

@@ -1,0 +1,209 @@
+// Host side of libspecverify: argument validation, workspace sizing, launches and
+// error reporting for the C ABI declared in specverify.h. Every check runs before any
+// HIP call, so an invalid call enqueues nothing (and needs no GPU to be rejected).
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "sv_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+sv_status fail(sv_status st, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+// SV_FAULT_INJECT=launch makes the next launch report a HIP failure without enqueuing,
+// so callers' error paths can be exercised from the host.
+bool inject_launch_fault() {
+    const char* e = std::getenv("SV_FAULT_INJECT");
+    return e && std::strcmp(e, "launch") == 0;
+}
+
+sv_status launched(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(SV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    g_err[0] = '\0';
+    return SV_OK;
+}
+
+bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+sv_status check_budget(const sv_budget_desc* d, const float* conf, const int32_t* keep,
+                       const int32_t* qo, const int32_t* sel) {
+    if (!d) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: desc is NULL");
+    if (d->num_reqs < 1 || d->num_reqs > SV_MAX_BUDGET_REQS)
+        return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: num_reqs %d outside [1, %d]", d->num_reqs, SV_MAX_BUDGET_REQS);
+    if (d->block < 1 || d->block > SV_MAX_BLOCK)
+        return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: block %d outside [1, %d]", d->block, SV_MAX_BLOCK);
+    const long long N = (long long)d->num_reqs * d->block;
+    if (N > SV_MAX_BUDGET_POSITIONS)
+        return fail(SV_ERR_UNSUPPORTED, "sv_alloc_budget: num_reqs*block = %lld above %d", N, SV_MAX_BUDGET_POSITIONS);
+    if (!keep || !qo || !sel) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: keep/qo_indptr/sel must not be NULL");
+    if (d->block > 1 && !conf) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: conf is NULL");
+    if (d->mode == SV_BUDGET_FIXED) {
+        if (d->fixed_budget < d->num_reqs || d->fixed_budget > N)
+            return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: fixed_budget %d outside [R=%d, R*b=%lld]",
+                        d->fixed_budget, d->num_reqs, N);
+    } else if (d->mode == SV_BUDGET_COST) {
+        if (d->num_ratios < 1 || d->num_ratios > SV_MAX_RATIOS)
+            return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: num_ratios %d outside [1, %d]", d->num_ratios, SV_MAX_RATIOS);
+        for (int j = 0; j < d->num_ratios; j++) {
+            if (d->ratio_permille[j] < 1 || d->ratio_permille[j] > 1000)
+                return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: ratio_permille[%d] = %d outside (0, 1000]", j,
+                            d->ratio_permille[j]);
+            if (j > 0 && d->ratio_permille[j] <= d->ratio_permille[j - 1])
+                return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: ratios must be strictly ascending");
+            if (d->cost[j] == 0) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: cost[%d] is 0", j);
+        }
+    } else {
+        return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: unknown mode %d", d->mode);
+    }
+    return SV_OK;
+}
+
+sv_status check_attn(const sv_attn_desc* d) {
+    if (!d) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: desc is NULL");
+    if (d->num_reqs < 1) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: num_reqs %d < 1", d->num_reqs);
+    if (d->block < 1 || d->block > SV_MAX_BLOCK)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: block %d outside [1, %d]", d->block, SV_MAX_BLOCK);
+    if (d->total_q_max < 1) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: total_q_max %d < 1", d->total_q_max);
+    if (d->num_q_heads < 1 || d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: num_q_heads %d is not a multiple of num_kv_heads %d",
+                    d->num_q_heads, d->num_kv_heads);
+    if (!is_pow2(d->page_size) || d->page_size > 4096)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: page_size %d is not a power of two <= 4096", d->page_size);
+    if (d->max_pages_per_req < 1 || d->num_pages < 1 || d->max_kv_len < 1)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: max_pages_per_req, num_pages and max_kv_len must be >= 1");
+    if ((long long)d->max_pages_per_req * d->page_size < d->max_kv_len)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: max_pages_per_req*page_size < max_kv_len");
+    if (!(d->sm_scale >= 0.0f) || std::isinf(d->sm_scale))
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: sm_scale must be finite and >= 0");
+    if (d->kv_split < 0 || d->kv_split % 64 != 0)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: kv_split %d is not a non-negative multiple of 64", d->kv_split);
+    const int G = d->num_q_heads / d->num_kv_heads;
+    if (d->dtype == SV_BF16) {
+        if (d->head_dim != 64 && d->head_dim != 128)
+            return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: bf16 head_dim %d (supported: 64, 128)", d->head_dim);
+        if ((long long)G * d->block > 256)
+            return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: group size * block = %d above 256", G * d->block);
+    } else if (d->dtype == SV_F32) {
+        if (d->head_dim < 4 || d->head_dim > 256 || d->head_dim % 4 != 0)
+            return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: fp32 head_dim %d (supported: multiples of 4 up to 256)",
+                        d->head_dim);
+    } else {
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: unknown dtype %d", d->dtype);
+    }
+    return SV_OK;
+}
+
+sv_status check_accept(const sv_accept_desc* d) {
+    if (!d) return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: desc is NULL");
+    if (d->num_reqs < 1) return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: num_reqs %d < 1", d->num_reqs);
+    if (d->block < 1 || d->block > SV_MAX_BLOCK)
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: block %d outside [1, %d]", d->block, SV_MAX_BLOCK);
+    if (d->vocab < 1 || d->vocab > SV_MAX_VOCAB)
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: vocab %d outside [1, %d]", d->vocab, SV_MAX_VOCAB);
+    if (d->dtype != SV_F32 && d->dtype != SV_BF16)
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: unknown dtype %d", d->dtype);
+    if (d->kind == SV_PROBS) {
+        if (d->dtype != SV_F32) return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: probability rows must be fp32");
+    } else if (d->kind == SV_LOGITS) {
+        if (!(d->temperature > 0.0f) || std::isinf(d->temperature))
+            return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: temperature must be finite and > 0");
+    } else {
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: unknown kind %d", d->kind);
+    }
+    if ((long long)d->num_reqs * d->block > (1LL << 30))
+        return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: too many rows");
+    return SV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t* keep,
+                          int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
+                          void* stream) {
+    sv_status st = check_budget(desc, conf, keep, qo_indptr, sel);
+    if (st != SV_OK) return st;
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_alloc_budget: injected launch failure");
+    return launched(sv::launch_budget(*desc, conf, keep, qo_indptr, sel, scores, utility, (hipStream_t)stream),
+                    "sv_alloc_budget");
+}
+
+size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc) {
+    if (check_attn(desc) != SV_OK) return 0;
+    const sv::AttnPlan p = sv::plan_attn(*desc);
+    return p.part_o_bytes + p.part_lse_bytes;
+}
+
+sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_cache,
+                         const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
+                         const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes,
+                         void* stream) {
+    sv_status st = check_attn(desc);
+    if (st != SV_OK) return st;
+    if (!q || !k_cache || !v_cache || !page_table || !qo_indptr || !kv_lens || !out)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: a required pointer is NULL");
+    const sv::AttnPlan p = sv::plan_attn(*desc);
+    const size_t need = p.part_o_bytes + p.part_lse_bytes;
+    if (need && (!ws || ws_bytes < need))
+        return fail(SV_ERR_WORKSPACE, "sv_verify_attn: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : (size_t)0);
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_verify_attn: injected launch failure");
+    return launched(sv::launch_attn(*desc, p, q, k_cache, v_cache, page_table, qo_indptr, kv_lens, out, lse, ws,
+                                    (hipStream_t)stream),
+                    "sv_verify_attn");
+}
+
+size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc) {
+    if (check_accept(desc) != SV_OK) return 0;
+    return sv::plan_accept(*desc).total;
+}
+
+sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const void* draft,
+                         const int32_t* draft_tokens, const int32_t* qo_indptr,
+                         const float* u_accept, const float* u_sample, int32_t* accept_len,
+                         int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
+                         void* stream) {
+    sv_status st = check_accept(desc);
+    if (st != SV_OK) return st;
+    const bool has_drafts = desc->block > 1;
+    if (!target || !qo_indptr || !u_sample || !accept_len || !out_tokens ||
+        (has_drafts && (!draft || !draft_tokens || !u_accept)))
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: a required pointer is NULL");
+    const sv::AcceptPlan p = sv::plan_accept(*desc);
+    if (!ws || ws_bytes < p.total)
+        return fail(SV_ERR_WORKSPACE, "sv_spec_accept: workspace of %zu bytes needed, %zu given", p.total,
+                    ws ? ws_bytes : (size_t)0);
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_spec_accept: injected launch failure");
+    return launched(sv::launch_accept(*desc, p, target, draft, draft_tokens, qo_indptr, u_accept, u_sample,
+                                      accept_len, out_tokens, flags, ws, (hipStream_t)stream),
+                    "sv_spec_accept");
+}
+
+const char* sv_status_string(int32_t status) {
+    switch (status) {
+        case SV_OK: return "SV_OK";
+        case SV_ERR_INVALID_ARG: return "SV_ERR_INVALID_ARG";
+        case SV_ERR_UNSUPPORTED: return "SV_ERR_UNSUPPORTED";
+        case SV_ERR_WORKSPACE: return "SV_ERR_WORKSPACE";
+        case SV_ERR_HIP: return "SV_ERR_HIP";
+        default: return "SV_UNKNOWN_STATUS";
+    }
+}
+
+const char* sv_last_error(void) { return g_err; }
+
+int32_t sv_abi_version(void) { return SV_ABI_VERSION; }
+
+}  // extern "C"

@@ -1,0 +1,46 @@
+// Internal declarations shared by the host API and the kernel translation units of
+// libspecverify. Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "specverify.h"
+
+namespace sv {
+
+// ---- budget -------------------------------------------------------------------
+hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* keep,
+                         int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
+                         hipStream_t stream);
+
+// ---- verify attention -----------------------------------------------------------
+struct AttnPlan {
+    int kv_split;     // tokens per split-KV work item (multiple of 64)
+    int max_splits;   // ceil(max_kv_len / kv_split)
+    int waves;        // waves per workgroup (bf16 path): 32 query rows per wave
+    size_t part_o_bytes;
+    size_t part_lse_bytes;
+};
+AttnPlan plan_attn(const sv_attn_desc& d);
+hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* q,
+                       const void* k_cache, const void* v_cache, const int32_t* page_table,
+                       const int32_t* qo_indptr, const int32_t* kv_lens, void* out, float* lse,
+                       void* ws, hipStream_t stream);
+
+// ---- acceptance -----------------------------------------------------------------
+struct AcceptPlan {
+    int stats_chunk;   // vocabulary elements per row-statistics workgroup
+    int stats_chunks;  // chunks per row
+    int res_chunk;     // vocabulary elements per residual workgroup
+    int res_chunks;
+    size_t off_stats_t, off_stats_q, off_plan, off_csum, total;
+};
+AcceptPlan plan_accept(const sv_accept_desc& d);
+hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const void* target,
+                         const void* draft, const int32_t* draft_tokens, const int32_t* qo_indptr,
+                         const float* u_accept, const float* u_sample, int32_t* accept_len,
+                         int32_t* out_tokens, int32_t* flags, void* ws, hipStream_t stream);
+
+}  // namespace sv

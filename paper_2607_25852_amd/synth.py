@@ -21,6 +21,8 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Optional
 
 import numpy as np
@@ -45,11 +47,14 @@ def _rng(seed: int, stream: int, index: int = 0) -> np.random.Generator:
 def bf16_bits(x: np.ndarray) -> np.ndarray:
     """fp32 -> bf16 bit patterns (uint16), round to nearest even; NaN stays NaN."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    rounded = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    u = x.view(np.uint32)
+    t = (u >> 16) & 1
+    t += u
+    t += 0x7FFF  # wraps only for NaN bit patterns, which are replaced below
+    t >>= 16
+    rounded = t.astype(np.uint16)
     nan = np.isnan(x)
     if nan.any():
-        rounded = rounded.copy()
         rounded[nan] = 0x7FC0
     return rounded
 
@@ -144,8 +149,10 @@ def indptr_from_depths(k: np.ndarray) -> np.ndarray:
 # logits, probabilities, draft tokens, confidences
 # ---------------------------------------------------------------------------
 def request_class(cfg: RoundConfig, i: int) -> Optional[int]:
+    """Difficulty class of request i: a seeded shuffle of a balanced round-robin
+    over the three classes (so every batch mixes them in equal shares)."""
     if cfg.logits[0] == "classes":
-        return int(_rng(cfg.seed, _S_CLASS, i).integers(0, 3))
+        return int(_rng(cfg.seed, _S_CLASS).permutation(np.arange(cfg.R) % 3)[i])
     if cfg.logits[0] == "class":
         return int(cfg.logits[1])
     return None
@@ -231,7 +238,8 @@ def make_logits_round(cfg: RoundConfig, want_probs: bool = False, requests=None)
     conf = np.empty((n, cfg.D), np.float32)
     tp = np.empty((n, cfg.b, cfg.V), np.float32) if want_probs else None
     dp = np.empty((n, cfg.D, cfg.V), np.float32) if want_probs else None
-    for k, i in enumerate(reqs):
+    def one(k_i):
+        k, i = k_i
         t32, d32 = request_logits(cfg, i)
         tfull[k] = encode(cfg, t32)
         dft[k] = encode(cfg, d32)
@@ -240,6 +248,10 @@ def make_logits_round(cfg: RoundConfig, want_probs: bool = False, requests=None)
         if want_probs:
             tp[k] = _softmax64(stored_as_f32(cfg, t32)).astype(np.float32)
             dp[k] = _softmax64(d_stored).astype(np.float32)
+
+    # every request has its own generators: parallel filling equals sequential filling
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        list(ex.map(one, enumerate(reqs)))
     out = dict(target_full=tfull, draft=dft, draft_tokens=toks, conf=conf)
     if want_probs:
         out.update(target_probs_full=tp, draft_probs=dp)
@@ -310,7 +322,8 @@ def make_kv(cfg: RoundConfig, L: np.ndarray, fill_unused=0.0, pool_slack=1.25, q
     fill = encode(cfg, np.array([fill_unused], np.float32))[0]
     kc = np.full((pool, Hkv, P, d), fill, st)
     vc = np.full((pool, Hkv, P, d), fill, st)
-    for i in range(R):
+
+    def fill(i):
         ntok = int(L[i]) + b
         kk = _rng(cfg.seed, _S_K, i).standard_normal((Hkv, ntok, d), dtype=np.float32)
         vv = _rng(cfg.seed, _S_V, i).standard_normal((Hkv, ntok, d), dtype=np.float32)
@@ -323,5 +336,10 @@ def make_kv(cfg: RoundConfig, L: np.ndarray, fill_unused=0.0, pool_slack=1.25, q
             cnt = min(P, ntok - lo)
             kc[pt[i, p], :, :cnt] = kk[:, lo:lo + cnt]
             vc[pt[i, p], :, :cnt] = vv[:, lo:lo + cnt]
+
+    # requests own disjoint pages and their own generators: filling them in parallel
+    # gives the same cache as filling them in order
+    with ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
+        list(ex.map(fill, range(R)))
     out.update(k_cache=kc, v_cache=vc)
     return out

@@ -1,0 +1,166 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the header
+declares, and rejects invalid calls on the host before anything is enqueued.
+NULL data pointers are used throughout, so no call here can reach a kernel launch
+even if a check were missing (the pointer checks would stop it first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_25852_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specverify.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2607_25852_amd import build
+        build.build()
+    return B.load()
+
+
+def test_header_declarations_are_exported(lib):
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = set(re.findall(r"\b(sv_[a-z_]+)\s*\(", text))
+    assert declared == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status_strings(lib):
+    assert lib.sv_abi_version() == 1
+    assert B.status_string(0) == "SV_OK"
+    assert B.status_string(3) == "SV_ERR_WORKSPACE"
+    assert B.status_string(99) == "SV_UNKNOWN_STATUS"
+
+
+def _budget(lib, d, conf=None):
+    return lib.sv_alloc_budget(ctypes.byref(d), conf, None, None, None, None, None, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(R=0, b=4, mode="fixed", fixed_budget=1), 1, "num_reqs"),
+    (dict(R=4097, b=1, mode="fixed", fixed_budget=4097), 1, "num_reqs"),
+    (dict(R=4, b=17, mode="fixed", fixed_budget=4), 1, "block"),
+    (dict(R=1024, b=16, mode="fixed", fixed_budget=1024), 2, "above 8192"),
+])
+def test_budget_descriptor_checks(lib, kw, status, msg):
+    d = B.budget_desc(**kw)
+    assert _budget(lib, d) == status
+    assert msg in B.last_error()
+
+
+def test_budget_argument_checks(lib):
+    fake = ctypes.c_void_p(16)
+    d = B.budget_desc(4, 8, "fixed", fixed_budget=3)
+    # NULL outputs are rejected first
+    assert _budget(lib, d) == 1 and "must not be NULL" in B.last_error()
+    def call(d):
+        return lib.sv_alloc_budget(ctypes.byref(d), None, fake, fake, fake, None, None, None)
+    assert call(d) == 1 and "conf" in B.last_error()  # conf NULL with b > 1
+    def call2(d):
+        return lib.sv_alloc_budget(ctypes.byref(d), None, None, None, None, None, None, None)
+    d = B.budget_desc(4, 8, "fixed", fixed_budget=33)
+    assert call2(d) == 1
+    d = B.budget_desc(4, 8, "cost", ratios_pm=(500, 250), cost=(1, 1))
+    assert call2(d) == 1
+    d = B.budget_desc(4, 8, "cost", ratios_pm=(250, 500), cost=(1, 0))
+    assert call2(d) == 1
+
+
+def _attn(lib, d, ws_bytes=0):
+    return lib.sv_verify_attn(ctypes.byref(d), None, None, None, None, None, None, None, None, None, ws_bytes,
+                              None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(Hq=8, Hkv=3), 1, "multiple"),
+    (dict(page_size=48), 1, "power of two"),
+    (dict(block=17), 1, "block"),
+    (dict(d=96), 2, "head_dim"),
+    (dict(Hq=64, Hkv=2), 2, "256"),  # G = 32, 32 * 16 rows
+    (dict(kv_split=100), 1, "kv_split"),
+    (dict(max_pages_per_req=2), 1, "max_pages_per_req*page_size"),
+    (dict(dtype=7), 1, "dtype"),
+])
+def test_attn_descriptor_checks(lib, kw, status, msg):
+    base = dict(R=4, total_q_max=64, block=16, Hq=32, Hkv=8, d=128, page_size=64, max_pages_per_req=130,
+                num_pages=1000, max_kv_len=8200, dtype=B.SV_BF16, kv_split=0)
+    base.update(kw)
+    d = B.attn_desc(**base)
+    assert _attn(lib, d) == status
+    assert msg in B.last_error()
+    assert lib.sv_verify_attn_workspace_size(ctypes.byref(d)) == 0
+
+
+def test_attn_workspace_size_and_null_pointers(lib):
+    d = B.attn_desc(64, 1024, 16, 64, 8, 128, 64, 520, 40000, 33000, B.SV_BF16)
+    n = lib.sv_verify_attn_workspace_size(ctypes.byref(d))
+    assert n > 0 and n % 4 == 0
+    assert _attn(lib, d) == 1 and "NULL" in B.last_error()
+
+
+def _accept(lib, d, ws=None, ws_bytes=0):
+    return lib.sv_spec_accept(ctypes.byref(d), None, None, None, None, None, None, None, None, None, ws, ws_bytes,
+                              None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(R=0), 1, "num_reqs"),
+    (dict(b=0), 1, "block"),
+    (dict(V=(1 << 22) + 1), 1, "vocab"),
+    (dict(kind=B.SV_PROBS, dtype=B.SV_BF16), 2, "fp32"),
+    (dict(temperature=0.0), 1, "temperature"),
+    (dict(temperature=float("nan")), 1, "temperature"),
+    (dict(kind=5), 1, "kind"),
+])
+def test_accept_descriptor_checks(lib, kw, status, msg):
+    base = dict(R=8, b=16, V=32768, kind=B.SV_LOGITS, dtype=B.SV_BF16, temperature=1.0)
+    base.update(kw)
+    d = B.accept_desc(**base)
+    assert _accept(lib, d) == status
+    assert msg in B.last_error()
+
+
+def test_accept_workspace_checks(lib):
+    d = B.accept_desc(8, 16, 32768, B.SV_LOGITS, B.SV_BF16)
+    need = lib.sv_spec_accept_workspace_size(ctypes.byref(d))
+    assert need > 0
+    assert _accept(lib, d) == 1 and "NULL" in B.last_error()
+
+
+def test_error_is_thread_local(lib):
+    import threading
+    d = B.accept_desc(0, 16, 100, B.SV_LOGITS, B.SV_F32)
+    assert _accept(lib, d) == 1
+    seen = []
+
+    def other():
+        seen.append(B.last_error())
+
+    t = threading.Thread(target=other)
+    t.start()
+    t.join()
+    assert seen == [""] and "num_reqs" in B.last_error()
+
+
+def test_injected_launch_failure_enqueues_nothing(lib, monkeypatch):
+    """SV_FAULT_INJECT=launch: a valid call reports SV_ERR_HIP from the host without
+    launching (the fake pointers below are never dereferenced)."""
+    monkeypatch.setenv("SV_FAULT_INJECT", "launch")
+    fake = ctypes.c_void_p(256)
+    d = B.budget_desc(4, 8, "fixed", fixed_budget=32)
+    st = lib.sv_alloc_budget(ctypes.byref(d), fake, fake, fake, fake, None, None, None)
+    assert st == B.SV_ERR_HIP and "injected" in B.last_error()
+    d = B.accept_desc(4, 8, 1024, B.SV_LOGITS, B.SV_F32)
+    need = lib.sv_spec_accept_workspace_size(ctypes.byref(d))
+    st = lib.sv_spec_accept(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, None, fake, need, None)
+    assert st == B.SV_ERR_HIP
+    # too-small workspace is reported before the injected failure
+    st = lib.sv_spec_accept(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, None, fake, need - 1,
+                            None)
+    assert st == B.SV_ERR_WORKSPACE

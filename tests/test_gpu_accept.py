@@ -1,0 +1,212 @@
+"""sv_spec_accept on the GPU against the oracle.
+
+Probability mode: identical fp32 probability rows and uniforms on both sides, so
+accepted lengths, committed tokens and flags must match bit for bit.
+Logits mode: the GPU computes softmax in fp32; outputs must match except where
+the oracle's own decision sits within a relative 1e-4 of its boundary or the
+draw within 1e-5*Z of a CDF step (counted, and required to be rare).
+"""
+import numpy as np
+import pytest
+
+from gpu_util import classify_accept, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_25852_amd import binding
+    binding.load()
+    return torch
+
+
+def gpu_accept(torch, target, draft, tokens, qo, ua, us, kind, dtype, T=1.0, repeat=1):
+    """target/draft: numpy fp32 or uint16 (bf16 bits)."""
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd.round import to_dev
+    R, D, V = draft.shape
+    b = D + 1
+    d = B.accept_desc(R, b, V, B.SV_PROBS if kind == "probs" else B.SV_LOGITS,
+                      B.SV_F32 if dtype == "f32" else B.SV_BF16, T)
+    ws = torch.empty(B.accept_workspace_size(d), dtype=torch.uint8, device="cuda")
+    tg, dr = to_dev(target), to_dev(draft)
+    tk, qd = to_dev(np.ascontiguousarray(tokens, np.int32)), to_dev(np.ascontiguousarray(qo, np.int32))
+    uad, usd = to_dev(np.ascontiguousarray(ua, np.float32)), to_dev(np.ascontiguousarray(us, np.float32))
+    outs = []
+    for _ in range(repeat):
+        acc = torch.full((R,), -9, dtype=torch.int32, device="cuda")
+        out = torch.full((R, b), -9, dtype=torch.int32, device="cuda")
+        flags = torch.full((R,), -9, dtype=torch.int32, device="cuda")
+        B.spec_accept(d, tg, dr, tk, qd, uad, usd, acc, out, flags, ws)
+        torch.cuda.synchronize()
+        outs.append(dict(accept_len=acc.cpu().numpy(), out_tokens=out.cpu().numpy(), flags=flags.cpu().numpy()))
+    return outs if repeat > 1 else outs[0]
+
+
+def assert_exact(g, o):
+    np.testing.assert_array_equal(g["accept_len"], o["accept_len"])
+    np.testing.assert_array_equal(g["out_tokens"], o["out_tokens"])
+    np.testing.assert_array_equal(g["flags"], o["flags"])
+
+
+def _workload(name, kind):
+    from paper_2607_25852_amd import synth
+    import oracle
+    cfg = synth.CONFIGS[name]
+    lr = synth.make_logits_round(cfg, want_probs=(kind == "probs"))
+    if cfg.budget[0] == "given":
+        qo = synth.indptr_from_depths(synth.given_depths(cfg))
+    elif cfg.budget[0] == "fixed":
+        qo = oracle.budget(lr["conf"], "fixed", fixed_budget=cfg.budget[1])["qo_indptr"]
+    else:
+        qo = oracle.budget(lr["conf"], "cost", cost=synth.profiled_cost(cfg.R, cfg.b))["qo_indptr"]
+    ua, us = synth.acceptance_uniforms(cfg)
+    if kind == "probs":
+        target = synth.pack_rows(lr["target_probs_full"], qo)
+        draft = lr["draft_probs"]
+        dtype = "f32"
+    else:
+        target = synth.pack_rows(lr["target_full"], qo)
+        draft = lr["draft"]
+        dtype = cfg.dtype
+    return cfg, target, draft, lr["draft_tokens"], qo, ua, us, dtype
+
+
+@pytest.mark.parametrize("name", ["tiny", "c16_b16", "c64_b16", "long_c32", "sweep_mtp_c64", "sweep_blk_c16"])
+def test_probs_mode_bit_exact(dev, orc, name):
+    say("accept probs", name)
+    cfg, target, draft, toks, qo, ua, us, dtype = _workload(name, "probs")
+    g = gpu_accept(dev, target, draft, toks, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, draft, toks, qo, ua, us, kind="probs")
+    assert_exact(g, o)
+    assert np.all(g["accept_len"] <= np.diff(qo) - 1)
+
+
+@pytest.mark.parametrize("name", ["tiny", "c16_b16", "c64_b16", "long_c32", "sweep_mtp_c32", "sweep_blk_c64"])
+def test_logits_mode_matches_oracle(dev, orc, name):
+    say("accept logits", name)
+    cfg, target, draft, toks, qo, ua, us, dtype = _workload(name, "logits")
+    g = gpu_accept(dev, target, draft, toks, qo, ua, us, "logits", dtype)
+    o = orc.accept(target, draft, toks, qo, ua, us, kind="logits", dtype=dtype, diagnostics=True)
+    exact, marginal, failures = classify_accept(g, o, ua)
+    say("accept logits", name, "exact", exact, "marginal", marginal, "fail", len(failures))
+    assert not failures, failures[:5]
+    assert marginal <= max(1, cfg.R // 50)
+    np.testing.assert_array_equal(g["flags"] & 4, o["flags"] & 4)
+
+
+def _rand_rows(rng, n, V, peaky=False):
+    x = rng.gamma(0.3 if peaky else 1.0, size=(n, V)) + 1e-6
+    return (x / x.sum(axis=-1, keepdims=True)).astype(np.float32)
+
+
+@pytest.mark.parametrize("V", [1, 2, 7, 1000, 1023, 8192, 8193, 40000])
+@pytest.mark.parametrize("b", [1, 2, 9, 16])
+def test_ragged_shapes_probs(dev, orc, V, b):
+    rng = np.random.default_rng(V * 17 + b)
+    R = 23
+    D = b - 1
+    k = rng.integers(1, b + 1, size=R)
+    qo = np.concatenate([[0], np.cumsum(k)]).astype(np.int32)
+    target = _rand_rows(rng, int(qo[-1]), V, peaky=True)
+    draft = _rand_rows(rng, R * max(D, 1), V, peaky=True).reshape(R, max(D, 1), V)[:, :D]
+    draft = np.ascontiguousarray(draft)
+    if D > 0:
+        toks = np.stack([[rng.choice(V, p=draft[i, t].astype(np.float64) / draft[i, t].astype(np.float64).sum())
+                          for t in range(D)] for i in range(R)]).astype(np.int32)
+    else:
+        toks = np.zeros((R, 0), np.int32)
+    ua = (rng.integers(0, 1 << 24, size=(R, D)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept ragged", V, b)
+    g = gpu_accept(dev, target, draft, toks, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, draft, toks, qo, ua, us, kind="probs")
+    assert_exact(g, o)
+
+
+@pytest.mark.parametrize("dtype,V,T", [("f32", 1000, 1.0), ("bf16", 4099, 1.0), ("bf16", 32768, 0.6),
+                                       ("f32", 8192, 1.7)])
+def test_ragged_logits(dev, orc, dtype, V, T):
+    from paper_2607_25852_amd import synth
+    rng = np.random.default_rng(V + int(T * 10))
+    R, b = 37, 12
+    D = b - 1
+    k = rng.integers(1, b + 1, size=R)
+    qo = np.concatenate([[0], np.cumsum(k)]).astype(np.int32)
+    tl = (rng.standard_normal((int(qo[-1]), V)) * 3).astype(np.float32)
+    dl = (rng.standard_normal((R, D, V)) * 3).astype(np.float32)
+    for i in range(R):  # drafts close to their target rows
+        n = k[i] - 1
+        dl[i, :n] = tl[qo[i]:qo[i] + n] + rng.standard_normal((n, V)).astype(np.float32) * 0.5
+    if dtype == "bf16":
+        tl, dl = synth.bf16_bits(tl), synth.bf16_bits(dl)
+    toks = rng.integers(0, V, size=(R, D)).astype(np.int32)
+    ua = (rng.integers(0, 1 << 24, size=(R, D)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept ragged logits", dtype, V, T)
+    g = gpu_accept(dev, tl, dl, toks, qo, ua, us, "logits", dtype, T)
+    o = orc.accept(tl, dl, toks, qo, ua, us, kind="logits", dtype=dtype, temperature=T, diagnostics=True)
+    exact, marginal, failures = classify_accept(g, o, ua)
+    assert not failures, failures[:5]
+    assert marginal <= 1
+
+
+def test_degenerate_rows(dev, orc):
+    """empty residual (fallback to p), all-zero row (no token), out-of-range and
+    NaN draft tokens, u = 0, one-hot rows, no drafts kept."""
+    V, b = 6, 4
+    D = b - 1
+    P = np.zeros((8, 4, V), np.float32)
+    Q = np.zeros((8, D, V), np.float32)
+    toks = np.zeros((8, D), np.int32)
+    ua = np.zeros((8, D), np.float32)
+    us = np.full(8, 0.6, np.float32)
+    P[:] = 1.0 / V
+    Q[:] = 1.0 / V
+    P[0, 0] = 0.5 / V                       # p <= q everywhere: empty residual after rejection
+    ua[0, 0] = 0.9
+    P[1, 0] = 0.0                           # all-zero: reject, empty residual, empty fallback
+    toks[2, 1] = 99                         # out-of-range token at draft 2
+    Q[3, 0, 2] = np.nan                     # NaN at the tested token
+    toks[3, 0] = 2
+    P[4, 0] = 0.0
+    P[4, 0, 5] = 1.0                        # one-hot target: always reject, yields 5
+    Q[5, 0] = 0.0
+    Q[5, 0, 1] = 1.0                        # one-hot draft
+    toks[5, 0] = 1
+    ua[5, 0] = 0.5
+    us[6] = 0.0                             # smallest uniform
+    us[7] = np.float32(1 - 2.0 ** -24)      # largest uniform
+    k = np.array([4, 4, 4, 4, 4, 4, 1, 4])
+    qo = np.concatenate([[0], np.cumsum(k)]).astype(np.int32)
+    target = np.concatenate([P[i, :k[i]] for i in range(8)])
+    g = gpu_accept(dev, target, Q, toks, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, Q, toks, qo, ua, us, kind="probs")
+    assert_exact(g, o)
+    assert g["flags"][0] == 1 and g["flags"][1] == 3 and g["flags"][2] & 4
+
+
+def test_all_positions_pruned(dev, orc):
+    """K = R: every request keeps only its certain position (plain decode step)."""
+    rng = np.random.default_rng(3)
+    R, b, V = 50, 16, 5000
+    qo = np.arange(R + 1, dtype=np.int32)
+    target = _rand_rows(rng, R, V)
+    draft = _rand_rows(rng, R * (b - 1), V).reshape(R, b - 1, V)
+    toks = rng.integers(0, V, size=(R, b - 1)).astype(np.int32)
+    ua = rng.random((R, b - 1)).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    g = gpu_accept(dev, target, draft, toks, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, draft, toks, qo, ua, us, kind="probs")
+    assert_exact(g, o)
+    assert np.all(g["accept_len"] == 0) and np.all(g["out_tokens"][:, 1:] == -1)
+
+
+def test_repeatable_bitwise(dev):
+    cfg_name = "c16_b16"
+    cfg, target, draft, toks, qo, ua, us, dtype = _workload(cfg_name, "logits")
+    a, b = gpu_accept(dev, target, draft, toks, qo, ua, us, "logits", dtype, repeat=2)
+    assert_exact(a, b)

@@ -1,0 +1,187 @@
+"""sv_verify_attn on the GPU against the fp64 oracle.
+
+Gate: max-abs <= 2e-2 (bf16) / 1e-5 (fp32) plus relative RMS <= 1e-2 (bf16) /
+1e-5 (fp32) and |lse difference| <= 1e-3 / 1e-5 -- at 64K-128K keys the outputs
+shrink to ~1/sqrt(L), so the max-abs gate alone would pass an all-zero output.
+Small workloads are compared on every (row, head); full-size ones on sampled
+(row, head) units covering every request, the first and last block row and
+every kv-head group.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from gpu_util import bf16_bits_of, compare_attention, f32_of_bits, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2607_25852_amd import binding
+    binding.load()
+    return torch
+
+
+def run_gpu_attn(torch, cfg, kv, qo, L, kv_split=0, block=None, sm_scale=0.0):
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd import synth
+    from paper_2607_25852_amd.round import to_dev
+    k = np.diff(qo)
+    R = cfg.R
+    q_rows = int(qo[-1])
+    q = synth.pack_rows(kv["q_full"], qo)
+    kv_lens = (L + k).astype(np.int32)
+    blk = block or cfg.b
+    d = B.attn_desc(R, q_rows, blk, cfg.Hq, cfg.Hkv, cfg.d, cfg.page, kv["page_table"].shape[1],
+                    kv["num_pages"], int(kv_lens.max()), B.SV_F32 if cfg.dtype == "f32" else B.SV_BF16,
+                    sm_scale=sm_scale, kv_split=kv_split)
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    out = torch.full((q_rows, cfg.Hq, cfg.d), float("nan"), dtype=dt, device="cuda")
+    lse = torch.full((q_rows, cfg.Hq), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(B.attn_workspace_size(d), 256), dtype=torch.uint8, device="cuda")
+    B.verify_attn(d, to_dev(q), to_dev(kv["k_cache"]), to_dev(kv["v_cache"]), to_dev(kv["page_table"]),
+                  to_dev(np.ascontiguousarray(qo, np.int32)), to_dev(kv_lens), out, lse, ws)
+    torch.cuda.synchronize()
+    o = out.float().cpu().numpy() if cfg.dtype == "bf16" else out.cpu().numpy()
+    return q, kv_lens, o.astype(np.float64), lse.cpu().numpy().astype(np.float64)
+
+
+def sample_units(qo, Hq, G, n_per_req, rng):
+    rows, heads = [], []
+    for i in range(len(qo) - 1):
+        r0, r1 = int(qo[i]), int(qo[i + 1])
+        cand_rows = [r0, r1 - 1] + list(rng.integers(r0, r1, size=max(0, n_per_req - 2)))
+        for j, r in enumerate(cand_rows):
+            rows.append(r)
+            heads.append(int((j * G + rng.integers(0, G)) % Hq) if j < Hq // G else int(rng.integers(0, Hq)))
+    return np.array(rows, np.int32), np.array(heads, np.int32)
+
+
+def check(orc, cfg, kv, qo, kv_lens, q, o_gpu, lse_gpu, units=None, scale=None):
+    ref_o, ref_l = orc.attention(q, kv["k_cache"], kv["v_cache"], kv["page_table"], qo, kv_lens,
+                                 dtype=cfg.dtype, units=units, scale=scale)
+    if units is None:
+        g_o = o_gpu.reshape(-1, cfg.d)
+        g_l = lse_gpu.reshape(-1)
+    else:
+        g_o = o_gpu[units[0], units[1]]
+        g_l = lse_gpu[units[0], units[1]]
+    ok, stats = compare_attention(g_o, g_l, ref_o, ref_l, cfg.dtype)
+    say("attn", cfg.name, stats)
+    assert ok, stats
+    return stats
+
+
+def _qo_for(cfg, orc=None):
+    from paper_2607_25852_amd import synth
+    import oracle
+    if cfg.budget[0] == "given":
+        return synth.indptr_from_depths(synth.given_depths(cfg))
+    conf = synth.make_logits_round(cfg)["conf"] if cfg.V <= 32768 else None
+    if cfg.budget[0] == "fixed":
+        return oracle.budget(conf, "fixed", fixed_budget=cfg.budget[1])["qo_indptr"]
+    rng = np.random.default_rng(cfg.seed)
+    return synth.indptr_from_depths(rng.integers(1, cfg.b + 1, size=cfg.R).astype(np.int32))
+
+
+def test_tiny_fp32_full(dev, orc):
+    from paper_2607_25852_amd import synth
+    cfg = synth.CONFIGS["tiny"]
+    L = synth.kv_context_lengths(cfg)
+    kv = synth.make_kv(cfg, L, fill_unused=np.nan)
+    qo = _qo_for(cfg)
+    say("attn tiny fp32")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l)
+
+
+@pytest.mark.parametrize("page,d,k_pattern", [(16, 64, "ragged"), (64, 128, "ragged"), (16, 128, "ones"),
+                                              (1, 64, "full"), (256, 128, "ragged")])
+def test_tiny_bf16_full(dev, orc, page, d, k_pattern):
+    from paper_2607_25852_amd import synth
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name=f"tiny_bf16_p{page}_d{d}", dtype="bf16", page=page, d=d)
+    L = synth.kv_context_lengths(cfg)
+    kv = synth.make_kv(cfg, L, fill_unused=np.nan)
+    k = {"ragged": np.array([8, 3, 1, 6]), "ones": np.ones(4, int), "full": np.full(4, 8)}[k_pattern]
+    qo = synth.indptr_from_depths(k)
+    say("attn tiny bf16", page, d, k_pattern)
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l)
+
+
+def test_c16_b16_full(dev, orc):
+    from paper_2607_25852_amd import synth
+    cfg = synth.CONFIGS["c16_b16"]
+    L = synth.kv_context_lengths(cfg)
+    kv = synth.make_kv(cfg, L, fill_unused=np.nan)
+    qo = _qo_for(cfg)
+    say("attn c16_b16")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    rows = np.repeat(np.arange(int(qo[-1])), cfg.Hq).astype(np.int32)
+    heads = np.tile(np.arange(cfg.Hq), int(qo[-1])).astype(np.int32)
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=(rows, heads))
+
+
+@pytest.mark.parametrize("name", ["c64_b16", "long_c32", "sweep_blk_c64", "sweep_mtp_c8"])
+def test_full_size_sampled(dev, orc, name):
+    from paper_2607_25852_amd import synth
+    cfg = synth.CONFIGS[name]
+    L = synth.kv_context_lengths(cfg)
+    say("attn gen", name)
+    kv = synth.make_kv(cfg, L)
+    qo = _qo_for(cfg)
+    say("attn run", name)
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    units = sample_units(qo, cfg.Hq, cfg.Hq // cfg.Hkv, 4, np.random.default_rng(1))
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=units)
+
+
+def test_peaky_queries_and_split_invariance(dev, orc):
+    """q scaled by 4 makes outputs O(1); results must not depend on the split size."""
+    from paper_2607_25852_amd import synth
+    cfg = dataclasses.replace(synth.CONFIGS["c16_b16"], name="c16_peaky", R=6)
+    L = synth.kv_context_lengths(synth.CONFIGS["c16_b16"])[:6]
+    kv = synth.make_kv(cfg, L, q_scale=4.0, fill_unused=np.nan)
+    qo = synth.indptr_from_depths(np.array([16, 1, 7, 16, 2, 11]))
+    outs = []
+    for split in (64, 320, 4096, 0):
+        say("attn split", split)
+        q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=split)
+        outs.append((o, l))
+    rows = np.repeat(np.arange(int(qo[-1])), cfg.Hq).astype(np.int32)
+    heads = np.tile(np.arange(cfg.Hq), int(qo[-1])).astype(np.int32)
+    st = check(orc, cfg, kv, qo, kvl, q, outs[0][0], outs[0][1], units=(rows, heads))
+    assert st["rel_rms"] < 1e-2
+    for o, l in outs[1:]:
+        assert np.abs(o - outs[0][0]).max() <= 2e-2
+        assert np.abs(l - outs[0][1]).max() <= 1e-3
+
+
+def test_context_free_block(dev, orc):
+    """L_i = 0: the block attends only to itself (row 0 sees one key)."""
+    from paper_2607_25852_amd import synth
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name="nolctx", dtype="bf16", kv=("list", 0, 0, 0, 0))
+    L = np.zeros(4, np.int32)
+    kv = synth.make_kv(cfg, L, fill_unused=np.nan)
+    qo = synth.indptr_from_depths(np.array([1, 8, 4, 2]))
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l)
+    # row 0 of request 0 sees exactly one key: output == its V row (rounded to bf16)
+    v0 = f32_of_bits(kv["v_cache"][kv["page_table"][0, 0], 0, 0]).astype(np.float64)
+    np.testing.assert_allclose(o[0, 0], v0, atol=1e-2)
+
+
+def test_repeatable_bitwise(dev):
+    from paper_2607_25852_amd import synth
+    cfg = dataclasses.replace(synth.CONFIGS["c16_b16"], name="rep", R=4)
+    L = synth.kv_context_lengths(synth.CONFIGS["c16_b16"])[:4]
+    kv = synth.make_kv(cfg, L)
+    qo = synth.indptr_from_depths(np.array([16, 5, 9, 1]))
+    a = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=256)
+    b = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=256)
+    np.testing.assert_array_equal(a[2], b[2])
+    np.testing.assert_array_equal(a[3], b[3])
