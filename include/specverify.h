@@ -118,7 +118,7 @@ sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t
 /* Sec. 4.1; the dense packed batch of Sec. 4.2).                             */
 /* ------------------------------------------------------------------------- */
 typedef struct {
-    int32_t num_reqs;          /* R >= 1                                            */
+    int32_t num_reqs;          /* R in [1, 65535]                                   */
     int32_t total_q_max;       /* rows allocated in q / out / lse (>= qo_indptr[R])  */
     int32_t block;             /* max k_i (<= 16)                                   */
     int32_t num_q_heads;       /* Hq                                               */
@@ -127,7 +127,7 @@ typedef struct {
     int32_t page_size;         /* P tokens per page, a power of two in [1, 4096]    */
     int32_t max_pages_per_req; /* columns of page_table                              */
     int32_t num_pages;         /* pages in each cache                                */
-    int32_t max_kv_len;        /* upper bound of kv_lens[i]                           */
+    int32_t max_kv_len;        /* upper bound of kv_lens[i], <= 2^22                  */
     int32_t dtype;             /* sv_dtype of q, caches and out                       */
     float sm_scale;            /* logit scale; 0 means 1/sqrt(d)                      */
     int32_t kv_split;          /* tokens per split-KV work item (multiple of 64), 0 = auto */
@@ -147,8 +147,9 @@ typedef struct {
  * page_table [R, max_pages_per_req] int32
  * qo_indptr  [R+1] int32 (1 <= k_i <= block), kv_lens [R] int32 (k_i <= kv_lens[i] <= max_kv_len)
  * out        [total_q_max, Hq, d] same dtype as q;  lse [total_q_max, Hq] fp32 or NULL
- * ws         scratch of at least sv_verify_attn_workspace_size(desc) bytes
- *            (partial results of split-KV work items), device memory.
+ * ws         scratch of at least sv_verify_attn_workspace_size(desc) bytes (bf16:
+ *            the work list of the persistent kernel and the partial results of
+ *            split-KV work items; fp32: none), device memory, overwritten by every call.
  * bf16 runs on MFMA with fp32 accumulation; fp32 runs on vector ALUs in fp32.
  */
 sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_cache,

@@ -42,7 +42,7 @@ struct AttnArgs {
     float* part_lse;  // [max_splits, total_q_max, Hq]  (log2 domain)
     int R, total_q, Hq, Hkv, G, block;
     int log2P, maxp, num_pages, max_kv_len;
-    int split, max_splits;
+    int split, max_splits, nrb;  // nrb: 128-row blocks per (request, kv-head)
     float scale_log2;  // sm_scale * log2(e)
     float scale;       // sm_scale
 };
@@ -60,25 +60,55 @@ __device__ inline uint16_t f2bf(float f) {
 // ---------------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ---------------------------------------------------------------------------------
-template <int HD>
-struct Lds {
-    static constexpr int kStride = HD + 8;       // K rows: HD bf16 + 16 B pad
-    static constexpr int vStride = kTile + 8;    // V^T rows: 64 tokens + 16 B pad
-    uint16_t k[2][kTile * kStride];
-    uint16_t vt[2][HD * vStride];
+// ---------------------------------------------------------------------------------
+// LDS tile layout: a 64-token tile of K and of V, each [token][HD] bf16, rows of HD*2
+// bytes with their 16-byte chunks XOR-swizzled: logical chunk c of token t sits at
+// position c ^ swz(t). swz swaps the two 2-bit fields of t % 16 so that (a) the 16
+// rows read together by one quarter-wave of the K-operand loads hit 16 different chunk
+// positions and (b) the 4 rows x 4 chunks read by one half-wave of the transpose reads
+// (two 16-lane groups) do too.
+// ---------------------------------------------------------------------------------
+__device__ __host__ inline int swz(int t) { return ((t & 3) << 2) | ((t >> 2) & 3); }
+
+template <int HD, int NBUF>
+struct LdsRing {
+    static constexpr int kTileBytes = kTile * HD * 2;  // one tensor
+    static constexpr int kMaxSlots = 1024;              // page-table entries of one split
+    uint16_t kv[NBUF][2][kTile * HD];                   // [buffer][K=0/V=1][token*HD + d]
+    int32_t pid[kMaxSlots];
 };
 
-template <int HD, int NW>
-__global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
-    constexpr int NT = NW * 64;
-    constexpr int CPR = HD / 8;                   // 16-byte chunks per token row
-    constexpr int CHUNKS = kTile * CPR;           // per tile, per tensor
-    constexpr int CPT = (CHUNKS + NT - 1) / NT;   // chunks per thread
-    constexpr int KK = HD / 16;                   // MFMA k-steps over the head dim
-    constexpr int DT = HD / 32;                   // output d-tiles
-    __shared__ Lds<HD> lds;
+// Asynchronous 16-byte-per-lane copy global -> LDS: lane l's 16 bytes land at
+// lds_base + 16*l. Issued from inline assembly so the compiler does not drain it
+// before every LDS read; completion is awaited explicitly with wait_vm<N>().
+__device__ inline void dma16(const void* gptr, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
+                 : "memory", "m0");
+}
+template <int N>
+__device__ inline void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
-    const int s = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// One work item (request i, kv-head h, split s, 128-row block rb). NBUF-deep LDS ring:
+// tile t is multiplied while tiles t+1 .. t+NBUF-1 stream in. Wave w owns query rows
+// 32*(w/2) .. +31 of the row block and token half w%2 of every tile (so a 64-row group
+// keeps all four SIMDs busy, two waves each); the two halves of a row group merge their
+// softmax states at the end. Every early return is uniform over the workgroup.
+template <int HD, int NW, int NBUF>
+__device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& lds, int i, int h, int s, int rb) {
+    constexpr int CPR = HD / 8;             // 16-byte chunks per token row
+    constexpr int TPS = 1024 / (HD * 2);    // tokens per 1 KB DMA segment
+    constexpr int NSEG = kTile / TPS;       // segments per tensor per tile
+    constexpr int IPW = 2 * NSEG / NW;      // DMA instructions per wave per tile
+    static_assert(IPW * NW == 2 * NSEG, "DMA split");
+    constexpr int KK = HD / 16;             // MFMA k-steps over the head dim
+    constexpr int DT = HD / 32;             // output d-tiles
+    constexpr int PF = NBUF - 1;            // prefetch distance in tiles
+
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int q0 = a.qo[i];
     const int k_i = a.qo[i + 1] - q0;
@@ -90,21 +120,32 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
     if (tok_begin >= kv_len) return;
     const int tok_end = min(kv_len, tok_begin + a.split);
     const int nsplit = (kv_len + a.split - 1) / a.split;
-    const int M = a.G * k_i;
+    const int M = a.G * k_i - rb * 128;  // rows of this row block
+    if (M <= 0) return;
+
+    // page ids of this split -> LDS (the host keeps a split within 1024 pages)
+    const int slot0 = tok_begin >> a.log2P;
+    const int nslots = ((tok_end - 1) >> a.log2P) - slot0 + 1;
+    const int32_t* __restrict__ pt = a.page_table + (size_t)i * a.maxp;
+    for (int e = tid; e < nslots; e += NW * 64) {
+        const int slot = slot0 + e;
+        const int pg = slot < a.maxp ? pt[slot] : -1;
+        lds.pid[e] = (pg >= 0 && pg < a.num_pages) ? pg : -1;
+    }
 
     // this lane's query row (N index of the MFMA) and its half (K-slice selector)
-    const int r = w * 32 + (lane & 31);
+    const int rg = w >> 1, th = w & 1;  // row group, token half of each tile
+    const int r = rg * 32 + (lane & 31);
     const int half = lane >> 5;
     const bool row_ok = r < M;
-    const int jq = row_ok ? r / a.G : 0;
-    const int head = h * a.G + (row_ok ? r % a.G : 0);
+    const int rr = rb * 128 + (row_ok ? r : 0);  // row within the request's kv-head group
+    const int jq = rr / a.G;
+    const int head = h * a.G + rr % a.G;
     const int limit = L + jq;  // last visible key of this row (inclusive)
 
     const uint16_t* __restrict__ qp = (const uint16_t*)a.q;
     const uint16_t* __restrict__ kcp = (const uint16_t*)a.kc;
     const uint16_t* __restrict__ vcp = (const uint16_t*)a.vc;
-    const int32_t* __restrict__ pt = a.page_table + (size_t)i * a.maxp;
-
     bf16x8 qf[KK];
     {
         const uint16_t* src = qp + ((size_t)(q0 + jq) * a.Hq + head) * HD;
@@ -114,135 +155,181 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
             qf[kk] = __builtin_bit_cast(bf16x8, v);
         }
     }
-
+    // the query fragments must have landed before the DMA ring starts: a wait the
+    // compiler sees (vmcnt(0)) keeps it from re-checking them inside the loop, where
+    // a vmcnt(0) would also drain the ring
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     f32x16 o[DT];
 #pragma unroll
     for (int t = 0; t < DT; t++) o[t] = f32x16{};
     float m_run = -1e30f, l_run = 0.0f;
 
-    // global -> register staging of one tile (K and V), zeros past the split end
-    u16x8 kreg[CPT], vreg[CPT];
-    auto load_tile = [&](int tb) {
+    const size_t head_off = (size_t)h << a.log2P;
+    const int pmask = (1 << a.log2P) - 1;
+    const uint32_t lds_ring = (uint32_t)(uintptr_t)&lds.kv[0][0][0];
+    __syncthreads();  // page ids visible
+
+    // DMA of one tile: wave w issues segments w*IPW .. w*IPW+IPW-1 of the 2*NSEG
+    // (K segments first, then V). Lane l of a segment moves token row t = seg*TPS + l/CPR,
+    // position l%CPR, fetching logical chunk (l%CPR) ^ swz(t). Tokens past the split end
+    // or on an invalid page read the first element of the cache (always present); they
+    // are masked out of the scores and zeroed in the V operand.
+    auto issue_tile = [&](int tile, int buf) {
+        const int tb = tok_begin + tile * kTile;
 #pragma unroll
-        for (int c = 0; c < CPT; c++) {
-            const int chunk = tid + c * NT;
-            u16x8 kv = {0, 0, 0, 0, 0, 0, 0, 0}, vv = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (chunk < CHUNKS) {
-                const int tok = tb + chunk / CPR;
-                const int dc = (chunk % CPR) * 8;
-                if (tok < tok_end) {
-                    const int slot = tok >> a.log2P;
-                    const int pg = slot < a.maxp ? pt[slot] : -1;
-                    if (pg >= 0 && pg < a.num_pages) {
-                        const size_t off = (((size_t)pg * a.Hkv + h) << a.log2P | (size_t)(tok & ((1 << a.log2P) - 1))) * HD + dc;
-                        kv = *(const u16x8*)(kcp + off);
-                        vv = *(const u16x8*)(vcp + off);
-                    }
-                }
-            }
-            kreg[c] = kv;
-            vreg[c] = vv;
-        }
-    };
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int c = 0; c < CPT; c++) {
-            const int chunk = tid + c * NT;
-            if (chunk < CHUNKS) {
-                const int t = chunk / CPR;
-                const int dc = (chunk % CPR) * 8;
-                *(u16x8*)&lds.k[buf][t * Lds<HD>::kStride + dc] = kreg[c];
-#pragma unroll
-                for (int e = 0; e < 8; e++) lds.vt[buf][(dc + e) * Lds<HD>::vStride + t] = vreg[c][e];
-            }
+        for (int k = 0; k < IPW; k++) {
+            const int n = w * IPW + k;
+            const int tensor = n / NSEG;
+            const int seg = n % NSEG;
+            const int t = seg * TPS + lane / CPR;
+            const int chunk = (lane % CPR) ^ (swz(t) & (CPR - 1));
+            const int tok = tb + t;
+            const int pg = lds.pid[min((tok >> a.log2P) - slot0, nslots - 1)];
+            const uint16_t* base = tensor ? vcp : kcp;
+            const uint16_t* src = (tok < tok_end && pg >= 0)
+                ? base + ((((size_t)pg * a.Hkv) << a.log2P) + head_off + (size_t)(tok & pmask)) * HD + chunk * 8
+                : base;
+            const uint32_t dst = lds_ring + (uint32_t)((buf * 2 + tensor) * LdsRing<HD, NBUF>::kTileBytes + seg * 1024);
+            dma16(src, __builtin_amdgcn_readfirstlane(dst));
         }
     };
 
-    const int ntiles = (tok_end - tok_begin + kTile - 1) / kTile;
-    load_tile(tok_begin);
-    store_tile(0);
-    __syncthreads();
-
-    for (int it = 0; it < ntiles; it++) {
-        const int buf = it & 1;
-        const int tb = tok_begin + it * kTile;
-        if (it + 1 < ntiles) load_tile(tb + kTile);
-
-        if (w * 32 < M) {
-            // S^T = K Q^T for two 32-token halves of the tile
-            f32x16 sacc[2];
+    auto compute_tile = [&](int buf, int tb) {
+        if (rg * 32 >= M) return;
+        const uint16_t* kt = lds.kv[buf][0];
+        const uint16_t* vt = lds.kv[buf][1];
+        // S^T = K Q^T for this wave's 32-token half of the tile
+        f32x16 sacc = f32x16{};
+        {
+            const int t = th * 32 + (lane & 31);
+            const uint16_t* krow = kt + t * HD;
+            const int sw = swz(t) & (CPR - 1);
 #pragma unroll
-            for (int tt = 0; tt < 2; tt++) {
-                f32x16 acc = f32x16{};
-                const uint16_t* krow = &lds.k[buf][(tt * 32 + (lane & 31)) * Lds<HD>::kStride + half * 8];
-#pragma unroll
-                for (int kk = 0; kk < KK; kk++) {
-                    const bf16x8 af = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow + kk * 16));
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], acc, 0, 0, 0);
-                }
-                sacc[tt] = acc;
+            for (int kk = 0; kk < KK; kk++) {
+                const bf16x8 af = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow + (((2 * kk + half) ^ sw) << 3)));
+                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc, 0, 0, 0);
             }
-            // scale, causal/tail mask (register e of half tt holds token 32tt + 8(e/4) + 4*half + e%4)
-            const bool need_mask = (tb + kTile - 1 > L) || (tb + kTile > tok_end) || !row_ok;
-            float mx = -INFINITY;
+        }
+        // scale, causal/tail mask (register e holds token 32th + 8(e/4) + 4*half + e%4)
+        const int tb_h = tb + th * 32;
+        const bool need_mask = (tb_h + 31 > L) || (tb_h + 32 > tok_end) || !row_ok;
+        float mx = -INFINITY;
 #pragma unroll
-            for (int tt = 0; tt < 2; tt++) {
-#pragma unroll
-                for (int e = 0; e < 16; e++) {
-                    float z = sacc[tt][e] * a.scale_log2;
-                    if (need_mask) {
-                        const int tok = tb + tt * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-                        if (!row_ok || tok > limit || tok >= tok_end) z = -INFINITY;
-                    }
-                    sacc[tt][e] = z;
-                    mx = fmaxf(mx, z);
-                }
+        for (int e = 0; e < 16; e++) {
+            float z = sacc[e] * a.scale_log2;
+            if (need_mask) {
+                const int tok = tb_h + 8 * (e >> 2) + 4 * half + (e & 3);
+                if (!row_ok || tok > limit || tok >= tok_end) z = -INFINITY;
             }
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float m_new = fmaxf(m_run, mx);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            float psum = 0.0f;
+            sacc[e] = z;
+            mx = fmaxf(mx, z);
+        }
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        float psum = 0.0f;
 #pragma unroll
-            for (int tt = 0; tt < 2; tt++)
-#pragma unroll
-                for (int e = 0; e < 16; e++) {
-                    const float p = __builtin_amdgcn_exp2f(sacc[tt][e] - m_new);
-                    sacc[tt][e] = p;
-                    psum += p;
-                }
-            l_run = l_run * alpha + psum;
-            m_run = m_new;
+        for (int e = 0; e < 16; e++) {
+            const float p = __builtin_amdgcn_exp2f(sacc[e] - m_new);
+            sacc[e] = p;
+            psum += p;
+        }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+        if (__any(alpha != 1.0f)) {
 #pragma unroll
             for (int t = 0; t < DT; t++) o[t] *= alpha;
+        }
+        const bool tail = tb_h + 32 > tok_end;  // V rows past the split end hold foreign data
 
-            // O^T += V^T P^T over four 16-token k-chunks
+        // O^T += V^T P^T over this half's two 16-token k-chunks. The V^T operand comes
+        // from two transpose reads: in 16-lane group g = lane/16, input lane j addresses
+        // token 16c + 8q + 4(g/2) + j/4 at dims 32t + 16(g%2) + 4(j%4) .. +3, and output
+        // lane j receives dim 32t + 16(g%2) + j of tokens 16c + 8q + 4(g/2) + 0..3.
+        const int g = lane >> 4, jl = lane & 15;
 #pragma unroll
-            for (int c = 0; c < 4; c++) {
-                bf16x8 pb;
+        for (int cc = 0; cc < 2; cc++) {
+            const int c = 2 * th + cc;
+            bf16x8 pb;
 #pragma unroll
-                for (int e = 0; e < 8; e++) pb[e] = (__bf16)sacc[c >> 1][8 * (c & 1) + e];
+            for (int e = 0; e < 8; e++) pb[e] = (__bf16)sacc[8 * cc + e];
 #pragma unroll
-                for (int t = 0; t < DT; t++) {
-                    const uint16_t* vrow = &lds.vt[buf][(t * 32 + (lane & 31)) * Lds<HD>::vStride + 16 * c + 4 * half];
-                    const uint64_t lo = *(const uint64_t*)vrow;
-                    const uint64_t hi = *(const uint64_t*)(vrow + 8);
-                    u16x8 vv;
+            for (int t = 0; t < DT; t++) {
+                i16x4 vq[2];
 #pragma unroll
-                    for (int e = 0; e < 4; e++) {
-                        vv[e] = (uint16_t)(lo >> (16 * e));
-                        vv[4 + e] = (uint16_t)(hi >> (16 * e));
-                    }
-                    o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, o[t], 0, 0, 0);
+                for (int qh = 0; qh < 2; qh++) {
+                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
+                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
+                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
+                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                    vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
                 }
+                if (tail) {
+#pragma unroll
+                    for (int qh = 0; qh < 2; qh++)
+#pragma unroll
+                        for (int e = 0; e < 4; e++)
+                            if (tb + 16 * c + 8 * qh + 4 * (g >> 1) + e >= tok_end) vq[qh][e] = 0;
+                }
+                const i16x4 lo = vq[0], hi = vq[1];
+                const u16x8 vv = {(uint16_t)lo[0], (uint16_t)lo[1], (uint16_t)lo[2], (uint16_t)lo[3],
+                                  (uint16_t)hi[0], (uint16_t)hi[1], (uint16_t)hi[2], (uint16_t)hi[3]};
+                o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, o[t], 0, 0, 0);
             }
         }
+    };
 
-        if (it + 1 < ntiles) store_tile(buf ^ 1);
+    // pipeline: before multiplying tile t, wait until its DMA (and only its) is done,
+    // barrier (tile t visible to all waves; tile t-1 no longer read), then refill the
+    // buffer of tile t-1 with tile t+PF.
+    const int ntiles = (tok_end - tok_begin + kTile - 1) / kTile;
+#pragma unroll
+    for (int t = 0; t < PF; t++)
+        if (t < ntiles) issue_tile(t, t);
+    for (int t = 0; t < ntiles; t++) {
+        const int newer = min(PF - 1, ntiles - 1 - t);  // tiles issued after t
+        if constexpr (PF >= 3) {
+            if (newer >= 2) wait_vm<2 * IPW>();
+            else if (newer == 1) wait_vm<IPW>();
+            else wait_vm<0>();
+        } else {
+            if (newer >= 1) wait_vm<IPW>();
+            else wait_vm<0>();
+        }
         __syncthreads();
+        if (t + PF < ntiles) issue_tile(t + PF, (t + PF) % NBUF);
+        compute_tile(t % NBUF, tok_begin + t * kTile);
     }
 
-    if (!row_ok) return;
-    const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    // merge the token halves of each row group: the odd wave parks (m, l, O) in LDS (the
+    // ring is free now), the even wave combines and writes. Both waves hold the same
+    // (row, dim) elements in the same lanes and registers.
+    float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    __syncthreads();
+    float* park = (float*)&lds.kv[0][0][0] + (size_t)rg * (64 * 16 * DT + 96);
+    const bool grp_ok = rg * 32 < M;
+    if (grp_ok && th == 1) {
+#pragma unroll
+        for (int t = 0; t < DT; t++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) park[(t * 16 + e) * 64 + lane] = o[t][e];
+        park[64 * 16 * DT + lane] = m_run;
+        if (lane < 32) park[64 * 16 * DT + 64 + lane] = l_tot;  // rows in lanes 0..31
+    }
+    __syncthreads();
+    if (!grp_ok || th == 1 || !row_ok) return;
+    {
+        const float m2 = park[64 * 16 * DT + lane];
+        const float l2 = park[64 * 16 * DT + 64 + (lane & 31)];
+        const float mm = fmaxf(m_run, m2);
+        const float a1 = __builtin_amdgcn_exp2f(m_run - mm), a2 = __builtin_amdgcn_exp2f(m2 - mm);
+#pragma unroll
+        for (int t = 0; t < DT; t++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) o[t][e] = o[t][e] * a1 + park[(t * 16 + e) * 64 + lane] * a2;
+        l_tot = l_tot * a1 + l2 * a2;
+        m_run = mm;
+    }
     const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
     const float lse2 = l_tot > 0.0f ? m_run + __log2f(l_tot) : -INFINITY;
     const size_t orow = (size_t)(q0 + jq) * a.Hq + head;
@@ -251,11 +338,11 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < DT; t++)
 #pragma unroll
-            for (int g = 0; g < 4; g++) {
-                const int dd = t * 32 + 8 * g + 4 * half;
+            for (int g2 = 0; g2 < 4; g2++) {
+                const int dd = t * 32 + 8 * g2 + 4 * half;
                 uint64_t pk = 0;
 #pragma unroll
-                for (int e = 0; e < 4; e++) pk |= (uint64_t)f2bf(o[t][4 * g + e] * inv) << (16 * e);
+                for (int e = 0; e < 4; e++) pk |= (uint64_t)f2bf(o[t][4 * g2 + e] * inv) << (16 * e);
                 *(uint64_t*)(op + dd) = pk;
             }
         if (a.lse && half == 0) a.lse[orow] = lse2 * kLn2;
@@ -264,14 +351,76 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int t = 0; t < DT; t++)
 #pragma unroll
-            for (int g = 0; g < 4; g++) {
-                const int dd = t * 32 + 8 * g + 4 * half;
-                f32x4 v = {o[t][4 * g] * inv, o[t][4 * g + 1] * inv, o[t][4 * g + 2] * inv, o[t][4 * g + 3] * inv};
+            for (int g2 = 0; g2 < 4; g2++) {
+                const int dd = t * 32 + 8 * g2 + 4 * half;
+                f32x4 v = {o[t][4 * g2] * inv, o[t][4 * g2 + 1] * inv, o[t][4 * g2 + 2] * inv, o[t][4 * g2 + 3] * inv};
                 *(f32x4*)(pp + dd) = v;
             }
         if (half == 0) a.part_lse[(size_t)s * a.total_q * a.Hq + orow] = lse2;
     }
 }
+
+// Plan of the persistent attention kernel: one entry (request << 16 | split) per split
+// of every valid request, the number of work items (entries x kv-heads x row blocks) and
+// a zeroed work counter. One workgroup; requests are scanned in chunks.
+__global__ __launch_bounds__(1024) void attn_plan_kernel(AttnArgs a, int32_t* groups, int32_t* ctr) {
+    __shared__ int wsum[16];
+    __shared__ int carry;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    if (tid == 0) carry = 0;
+    __syncthreads();
+    for (int base = 0; base < a.R; base += 1024) {
+        const int i = base + tid;
+        int ns = 0;
+        if (i < a.R) {
+            const int q0 = a.qo[i], k_i = a.qo[i + 1] - q0;
+            int kv_len = a.kv_lens[i];
+            if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
+            if (k_i >= 1 && k_i <= a.block && kv_len - k_i >= 0 && q0 >= 0 && q0 + k_i <= a.total_q)
+                ns = (kv_len + a.split - 1) / a.split;
+        }
+        int incl = ns;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(incl, off, 64);
+            if (lane >= off) incl += v;
+        }
+        if (lane == 63) wsum[w] = incl;
+        __syncthreads();
+        int pre = carry;
+        for (int k = 0; k < w; k++) pre += wsum[k];
+        const int start = pre + incl - ns;
+        for (int t = 0; t < ns; t++) groups[start + t] = (i << 16) | t;
+        __syncthreads();
+        if (tid == 1023) carry = start + ns;
+        __syncthreads();
+    }
+    if (tid == 0) {
+        ctr[0] = carry * a.Hkv * a.nrb;
+        ctr[1] = 0;
+    }
+}
+
+// Persistent: one workgroup per CU pulls work items from the counter until the list is
+// exhausted (every wave leaves through the same test).
+template <int HD, int NW, int NBUF>
+__global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ groups,
+                                                               int32_t* __restrict__ ctr) {
+    __shared__ __attribute__((aligned(16))) LdsRing<HD, NBUF> lds;
+    __shared__ int s_item;
+    const int nitems = ctr[0];
+    const int per_group = a.Hkv * a.nrb;
+    for (;;) {
+        if (threadIdx.x == 0) s_item = atomicAdd(&ctr[1], 1);
+        __syncthreads();
+        const int item = s_item;
+        __syncthreads();
+        if (item >= nitems) break;
+        const int gv = groups[item / per_group];
+        const int within = item % per_group;
+        attn_item<HD, NW, NBUF>(a, lds, gv >> 16, within / a.nrb, gv & 0xFFFF, within % a.nrb);
+    }
+}
+
 
 // merge split partials: one wavefront per (row, head); lanes over d
 template <int HD, bool BF16OUT>
@@ -419,7 +568,8 @@ int ilog2(int x) {
 AttnPlan plan_attn(const sv_attn_desc& d) {
     AttnPlan p{};
     const int maxM = (d.num_q_heads / d.num_kv_heads) * d.block;
-    p.waves = maxM <= 64 ? 2 : (maxM <= 128 ? 4 : 8);
+    p.waves = 8;  // (32-row group, token half) per wave: 128 query rows per workgroup
+    p.row_blocks = (maxM + 127) / 128;
     if (d.dtype == SV_F32) {
         p.kv_split = 0;
         p.max_splits = 1;
@@ -427,13 +577,18 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     }
     int split = d.kv_split;
     if (split <= 0) {
-        // aim for ~2048 work items over the worst case (every request at max_kv_len)
-        const long long work = (long long)d.num_reqs * d.num_kv_heads;
-        long long want = (long long)d.max_kv_len * work / 2048;
+        // at most ~16 splits for the longest request, 1024..8192 tokens each: enough work
+        // items to balance 256 CUs, few enough that the partial results stay small
+        long long want = ((long long)d.max_kv_len + 15) / 16;
         if (want < 1024) want = 1024;
+        if (want > 8192) want = 8192;
         split = (int)(((want + 63) / 64) * 64);
     }
     if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
+    // a split's page ids are staged in LDS: at most 1024 pages per split (a split of
+    // n tokens starting on a 64-token boundary touches at most n / P + 2 pages)
+    const long long max_split = 1022LL * d.page_size;
+    if (split > max_split) split = (int)(max_split / 64 * 64);
     if (split < 64) split = 64;
     p.kv_split = split;
     p.max_splits = (d.max_kv_len + split - 1) / split;
@@ -442,6 +597,10 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
         p.part_o_bytes = (size_t)p.max_splits * d.total_q_max * d.num_q_heads * d.head_dim * sizeof(float);
         p.part_lse_bytes = (size_t)p.max_splits * d.total_q_max * d.num_q_heads * sizeof(float);
     }
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    p.off_groups = al(p.part_o_bytes + p.part_lse_bytes);
+    p.off_ctr = al(p.off_groups + (size_t)d.num_reqs * p.max_splits * sizeof(int32_t));
+    p.ws_bytes = p.off_ctr + 2 * sizeof(int32_t);
     return p;
 }
 
@@ -480,18 +639,28 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
         hipLaunchKernelGGL(attn_f32_kernel, dim3((units + 3) / 4), dim3(256), 0, stream, a, d.head_dim);
         return hipGetLastError();
     }
-    const dim3 grid(plan.max_splits, d.num_kv_heads, d.num_reqs);
-#define SV_LAUNCH_ATTN(HDV, NWV) \
-    hipLaunchKernelGGL((attn_bf16_kernel<HDV, NWV>), grid, dim3(NWV * 64), 0, stream, a)
-    if (d.head_dim == 128) {
-        if (plan.waves == 2) SV_LAUNCH_ATTN(128, 2);
-        else if (plan.waves == 4) SV_LAUNCH_ATTN(128, 4);
-        else SV_LAUNCH_ATTN(128, 8);
-    } else {
-        if (plan.waves == 2) SV_LAUNCH_ATTN(64, 2);
-        else if (plan.waves == 4) SV_LAUNCH_ATTN(64, 4);
-        else SV_LAUNCH_ATTN(64, 8);
+    a.nrb = plan.row_blocks;
+    // persistent grid: one workgroup per compute unit of the current device
+    static int cu_count[64] = {0};
+    int dev = 0;
+    hipError_t e0 = hipGetDevice(&dev);
+    if (e0 != hipSuccess) return e0;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (cu_count[dev] == 0) {
+        int n = 0;
+        e0 = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+        if (e0 != hipSuccess) return e0;
+        cu_count[dev] = n > 0 ? n : 1;
     }
+    char* wsb = (char*)ws;
+    int32_t* groups = (int32_t*)(wsb + plan.off_groups);
+    int32_t* ctr = (int32_t*)(wsb + plan.off_ctr);
+    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, stream, a, groups, ctr);
+    const dim3 grid(cu_count[dev]);
+#define SV_LAUNCH_ATTN(HDV, NWV) \
+    hipLaunchKernelGGL((attn_bf16_kernel<HDV, NWV, 4>), grid, dim3(NWV * 64), 0, stream, a, groups, ctr)
+    if (d.head_dim == 128) SV_LAUNCH_ATTN(128, 8);
+    else SV_LAUNCH_ATTN(64, 8);
 #undef SV_LAUNCH_ATTN
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.max_splits <= 1) return e;

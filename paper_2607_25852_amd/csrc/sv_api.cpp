@@ -71,7 +71,10 @@ sv_status check_budget(const sv_budget_desc* d, const float* conf, const int32_t
 
 sv_status check_attn(const sv_attn_desc* d) {
     if (!d) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: desc is NULL");
-    if (d->num_reqs < 1) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: num_reqs %d < 1", d->num_reqs);
+    if (d->num_reqs < 1 || d->num_reqs > 65535)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: num_reqs %d outside [1, 65535]", d->num_reqs);
+    if (d->max_kv_len > (1 << 22))
+        return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: max_kv_len %d above 2^22", d->max_kv_len);
     if (d->block < 1 || d->block > SV_MAX_BLOCK)
         return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: block %d outside [1, %d]", d->block, SV_MAX_BLOCK);
     if (d->total_q_max < 1) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: total_q_max %d < 1", d->total_q_max);
@@ -92,8 +95,8 @@ sv_status check_attn(const sv_attn_desc* d) {
     if (d->dtype == SV_BF16) {
         if (d->head_dim != 64 && d->head_dim != 128)
             return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: bf16 head_dim %d (supported: 64, 128)", d->head_dim);
-        if ((long long)G * d->block > 256)
-            return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: group size * block = %d above 256", G * d->block);
+        if ((long long)G * d->block > 1024)
+            return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: group size * block = %d above 1024", G * d->block);
     } else if (d->dtype == SV_F32) {
         if (d->head_dim < 4 || d->head_dim > 256 || d->head_dim % 4 != 0)
             return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: fp32 head_dim %d (supported: multiples of 4 up to 256)",
@@ -142,8 +145,7 @@ sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t
 
 size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc) {
     if (check_attn(desc) != SV_OK) return 0;
-    const sv::AttnPlan p = sv::plan_attn(*desc);
-    return p.part_o_bytes + p.part_lse_bytes;
+    return sv::plan_attn(*desc).ws_bytes;
 }
 
 sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_cache,
@@ -155,7 +157,7 @@ sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_
     if (!q || !k_cache || !v_cache || !page_table || !qo_indptr || !kv_lens || !out)
         return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: a required pointer is NULL");
     const sv::AttnPlan p = sv::plan_attn(*desc);
-    const size_t need = p.part_o_bytes + p.part_lse_bytes;
+    const size_t need = p.ws_bytes;
     if (need && (!ws || ws_bytes < need))
         return fail(SV_ERR_WORKSPACE, "sv_verify_attn: workspace of %zu bytes needed, %zu given", need,
                     ws ? ws_bytes : (size_t)0);

@@ -19,9 +19,13 @@ hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* ke
 struct AttnPlan {
     int kv_split;     // tokens per split-KV work item (multiple of 64)
     int max_splits;   // ceil(max_kv_len / kv_split)
-    int waves;        // waves per workgroup (bf16 path): 32 query rows per wave
-    size_t part_o_bytes;
-    size_t part_lse_bytes;
+    int waves;        // waves per workgroup (bf16 path)
+    int row_blocks;   // 128-query-row blocks per (request, kv-head)
+    size_t part_o_bytes;    // split partial outputs (fp32), offset 0
+    size_t part_lse_bytes;  // split partial log-sum-exps, after part_o
+    size_t off_groups;      // work list of the persistent kernel
+    size_t off_ctr;         // {number of work items, work counter}
+    size_t ws_bytes;        // total workspace (0 for the fp32 path)
 };
 AttnPlan plan_attn(const sv_attn_desc& d);
 hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* q,

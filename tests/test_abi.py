@@ -82,7 +82,7 @@ def _attn(lib, d, ws_bytes=0):
     (dict(page_size=48), 1, "power of two"),
     (dict(block=17), 1, "block"),
     (dict(d=96), 2, "head_dim"),
-    (dict(Hq=64, Hkv=2), 2, "256"),  # G = 32, 32 * 16 rows
+    (dict(Hq=128, Hkv=1), 2, "1024"),  # G = 128, 128 * 16 rows
     (dict(kv_split=100), 1, "kv_split"),
     (dict(max_pages_per_req=2), 1, "max_pages_per_req*page_size"),
     (dict(dtype=7), 1, "dtype"),
