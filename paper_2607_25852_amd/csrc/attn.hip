@@ -85,6 +85,12 @@ __device__ inline void dma16(const void* gptr, uint32_t lds_base) {
     asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
                  : "memory", "m0");
 }
+// Same copy with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane byte offset.
+__device__ inline void dma16s(uint32_t voff, const void* sbase, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+                 "s"(lds_base)
+                 : "memory", "m0");
+}
 template <int N>
 __device__ inline void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -98,7 +104,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // 32*(w/2) .. +31 of the row block and token half w%2 of every tile (so a 64-row group
 // keeps all four SIMDs busy, two waves each); the two halves of a row group merge their
 // softmax states at the end. Every early return is uniform over the workgroup.
-template <int HD, int NW, int NBUF>
+template <int HD, int NW, int NBUF, bool ONEPAGE>
 __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& lds, int i, int h, int s, int rb) {
     constexpr int CPR = HD / 8;             // 16-byte chunks per token row
     constexpr int TPS = 1024 / (HD * 2);    // tokens per 1 KB DMA segment
@@ -171,26 +177,47 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
 
     // DMA of one tile: wave w issues segments w*IPW .. w*IPW+IPW-1 of the 2*NSEG
     // (K segments first, then V). Lane l of a segment moves token row t = seg*TPS + l/CPR,
-    // position l%CPR, fetching logical chunk (l%CPR) ^ swz(t). Tokens past the split end
-    // or on an invalid page read the first element of the cache (always present); they
-    // are masked out of the scores and zeroed in the V operand.
+    // position l%CPR, fetching logical chunk (l%CPR) ^ swz(t); the per-lane byte offset of
+    // that chunk inside the tile is loop-invariant.
+    // ONEPAGE (page size >= 64): a 64-token tile lies inside one page, so each tile needs
+    // one wave-uniform base address; an invalid page reads page 0 (always present).
+    // Otherwise every lane looks its page up; tokens past the split end or on an invalid
+    // page read the first element of the cache. Either way such tokens are masked out of
+    // the scores and zeroed in the V operand.
+    uint32_t voff[IPW], ldsoff[IPW];
+    int tk[IPW];
+#pragma unroll
+    for (int k = 0; k < IPW; k++) {
+        const int n = w * IPW + k;
+        const int seg = n % NSEG;
+        const int t = seg * TPS + lane / CPR;
+        tk[k] = t;
+        voff[k] = (uint32_t)(t * HD + (((lane % CPR) ^ (swz(t) & (CPR - 1))) << 3)) * 2u;
+        ldsoff[k] = (uint32_t)__builtin_amdgcn_readfirstlane((n / NSEG) * LdsRing<HD, NBUF>::kTileBytes + seg * 1024);
+    }
+    const int my_tensor = __builtin_amdgcn_readfirstlane((w * IPW) / NSEG);  // a wave moves one tensor
+    const uint16_t* cbase = my_tensor ? vcp : kcp;
     auto issue_tile = [&](int tile, int buf) {
         const int tb = tok_begin + tile * kTile;
+        const uint32_t lbuf = lds_ring + (uint32_t)(buf * 2 * LdsRing<HD, NBUF>::kTileBytes);
+        if constexpr (ONEPAGE) {
+            const int pg = __builtin_amdgcn_readfirstlane(lds.pid[(tb >> a.log2P) - slot0]);
+            const uint16_t* base = pg >= 0
+                ? cbase + ((((size_t)pg * a.Hkv) << a.log2P) + head_off + (size_t)(tb & pmask)) * HD
+                : cbase + (size_t)(tb & pmask) * HD;
 #pragma unroll
-        for (int k = 0; k < IPW; k++) {
-            const int n = w * IPW + k;
-            const int tensor = n / NSEG;
-            const int seg = n % NSEG;
-            const int t = seg * TPS + lane / CPR;
-            const int chunk = (lane % CPR) ^ (swz(t) & (CPR - 1));
-            const int tok = tb + t;
-            const int pg = lds.pid[min((tok >> a.log2P) - slot0, nslots - 1)];
-            const uint16_t* base = tensor ? vcp : kcp;
-            const uint16_t* src = (tok < tok_end && pg >= 0)
-                ? base + ((((size_t)pg * a.Hkv) << a.log2P) + head_off + (size_t)(tok & pmask)) * HD + chunk * 8
-                : base;
-            const uint32_t dst = lds_ring + (uint32_t)((buf * 2 + tensor) * LdsRing<HD, NBUF>::kTileBytes + seg * 1024);
-            dma16(src, __builtin_amdgcn_readfirstlane(dst));
+            for (int k = 0; k < IPW; k++) dma16s(voff[k], base, lbuf + ldsoff[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < IPW; k++) {
+                const int tok = tb + tk[k];
+                const int pg = lds.pid[min((tok >> a.log2P) - slot0, nslots - 1)];
+                const uint16_t* src = (tok < tok_end && pg >= 0)
+                    ? cbase + ((((size_t)pg * a.Hkv) << a.log2P) + head_off + (size_t)(tok & pmask)) * HD
+                          + (voff[k] / 2 - tk[k] * HD)
+                    : cbase;
+                dma16(src, lbuf + ldsoff[k]);
+            }
         }
     };
 
@@ -198,7 +225,7 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
         if (rg * 32 >= M) return;
         const uint16_t* kt = lds.kv[buf][0];
         const uint16_t* vt = lds.kv[buf][1];
-        // S^T = K Q^T for this wave's 32-token half of the tile
+        // S^T = K Q^T for this wave's 32-token half of the tile (unscaled)
         f32x16 sacc = f32x16{};
         {
             const int t = th * 32 + (lane & 31);
@@ -210,36 +237,42 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
                 sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc, 0, 0, 0);
             }
         }
-        // scale, causal/tail mask (register e holds token 32th + 8(e/4) + 4*half + e%4)
+        // causal/tail mask on the raw scores (register e holds token 32th + 8(e/4) + 4*half + e%4)
         const int tb_h = tb + th * 32;
         const bool need_mask = (tb_h + 31 > L) || (tb_h + 32 > tok_end) || !row_ok;
-        float mx = -INFINITY;
+        if (need_mask) {
 #pragma unroll
-        for (int e = 0; e < 16; e++) {
-            float z = sacc[e] * a.scale_log2;
-            if (need_mask) {
+            for (int e = 0; e < 16; e++) {
                 const int tok = tb_h + 8 * (e >> 2) + 4 * half + (e & 3);
-                if (!row_ok || tok > limit || tok >= tok_end) z = -INFINITY;
+                if (!row_ok || tok > limit || tok >= tok_end) sacc[e] = -INFINITY;
             }
-            sacc[e] = z;
-            mx = fmaxf(mx, z);
         }
+        float mx = fmaxf(fmaxf(sacc[0], sacc[1]), sacc[2]);
+#pragma unroll
+        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[e]), sacc[e + 1]);
+        mx = fmaxf(mx, sacc[15]);
         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        const float mxs = mx * a.scale_log2;  // tile max in scaled log2 units (-inf: all masked)
+        // lazy rescale: the running max moves only when a score exceeds it by more than 8,
+        // so p = 2^(z - m) <= 256 stays exact in fp32 and bf16, and most tiles skip the
+        // rescale of the accumulators
+        if (__any(mxs > m_run + 8.0f)) {
+            const float m_new = fmaxf(m_run, mxs);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int t = 0; t < DT; t++) o[t] *= alpha;
+            m_run = m_new;
+        }
+        const float nm = -m_run;
         float psum = 0.0f;
 #pragma unroll
         for (int e = 0; e < 16; e++) {
-            const float p = __builtin_amdgcn_exp2f(sacc[e] - m_new);
+            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, nm));
             sacc[e] = p;
             psum += p;
         }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-        if (__any(alpha != 1.0f)) {
-#pragma unroll
-            for (int t = 0; t < DT; t++) o[t] *= alpha;
-        }
+        l_run += psum;
         const bool tail = tb_h + 32 > tok_end;  // V rows past the split end hold foreign data
 
         // O^T += V^T P^T over this half's two 16-token k-chunks. The V^T operand comes
@@ -402,7 +435,7 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnArgs a, int32_t* gr
 
 // Persistent: one workgroup per CU pulls work items from the counter until the list is
 // exhausted (every wave leaves through the same test).
-template <int HD, int NW, int NBUF>
+template <int HD, int NW, int NBUF, bool ONEPAGE>
 __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ groups,
                                                                int32_t* __restrict__ ctr) {
     __shared__ __attribute__((aligned(16))) LdsRing<HD, NBUF> lds;
@@ -417,7 +450,7 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
         if (item >= nitems) break;
         const int gv = groups[item / per_group];
         const int within = item % per_group;
-        attn_item<HD, NW, NBUF>(a, lds, gv >> 16, within / a.nrb, gv & 0xFFFF, within % a.nrb);
+        attn_item<HD, NW, NBUF, ONEPAGE>(a, lds, gv >> 16, within / a.nrb, gv & 0xFFFF, within % a.nrb);
     }
 }
 
@@ -657,10 +690,16 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
     int32_t* ctr = (int32_t*)(wsb + plan.off_ctr);
     hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, stream, a, groups, ctr);
     const dim3 grid(cu_count[dev]);
-#define SV_LAUNCH_ATTN(HDV, NWV) \
-    hipLaunchKernelGGL((attn_bf16_kernel<HDV, NWV, 4>), grid, dim3(NWV * 64), 0, stream, a, groups, ctr)
-    if (d.head_dim == 128) SV_LAUNCH_ATTN(128, 8);
-    else SV_LAUNCH_ATTN(64, 8);
+#define SV_LAUNCH_ATTN(HDV, NWV, ONEP) \
+    hipLaunchKernelGGL((attn_bf16_kernel<HDV, NWV, 4, ONEP>), grid, dim3(NWV * 64), 0, stream, a, groups, ctr)
+    const bool onepage = d.page_size >= kTile;
+    if (d.head_dim == 128) {
+        if (onepage) SV_LAUNCH_ATTN(128, 8, true);
+        else SV_LAUNCH_ATTN(128, 8, false);
+    } else {
+        if (onepage) SV_LAUNCH_ATTN(64, 8, true);
+        else SV_LAUNCH_ATTN(64, 8, false);
+    }
 #undef SV_LAUNCH_ATTN
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.max_splits <= 1) return e;
