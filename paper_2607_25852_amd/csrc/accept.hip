@@ -10,10 +10,10 @@
 //             acceptance test of every draft in its own lane (exact fp64 product
 //             u*q < p), finds the first rejection with a ballot, writes the accepted
 //             prefix and the plan of the extra-token draw.
-//   ressum    per (request, vocabulary chunk): integer weights floor(r * 2^40) of the
-//             residual max(p - q, 0) (or of p for the bonus) and their chunk sums.
-//   search    per request: Z = sum of chunk sums, threshold floor(m * Z / 2^24), the
-//             chunk holding it, then the exact token inside that chunk.
+//   chunksum  per (request, vocabulary chunk): the integer weights floor(r * 2^40) of the
+//             residual max(p - q, 0) (or of p for the bonus), summed over the chunk.
+//   search    per request: Z, the threshold floor(m * Z / 2^24), the chunk holding it and
+//             the exact token inside that chunk.
 // Every sum that decides a token is an integer sum, so the result does not depend on
 // how the vocabulary is split across threads.
 #include "sv_internal.h"
@@ -71,10 +71,18 @@ __device__ inline float prob_of(const T* row, int v, float m, float iS, float in
     }
 }
 
+// floor(min(r, 1) * 2^40) for r > 0 (0 for r <= 0 or NaN), from the fp32 bits: a normal
+// r is m * 2^(e - 150) with m the 24-bit significand and e the biased exponent, so
+// r * 2^40 = m * 2^(e - 110); subnormals give less than 2^-86, i.e. 0.
 __device__ inline uint64_t weight_of(float r) {
     if (!(r > 0.0f)) return 0;
-    if (r > 1.0f) r = 1.0f;
-    return (uint64_t)(r * 1099511627776.0f);  // exact: power-of-two scaling
+    if (r >= 1.0f) return 1ull << 40;
+    const uint32_t u = __float_as_uint(r);
+    const int e = (int)(u >> 23);
+    if (e == 0) return 0;
+    const uint64_t m = (uint64_t)((u & 0x7FFFFFu) | 0x800000u);
+    const int sh = e - 110;  // <= 16 because r < 1
+    return sh >= 0 ? (m << sh) : (sh > -64 ? (m >> -sh) : 0);
 }
 
 template <typename T>
@@ -157,13 +165,27 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
     }
 }
 
+// combine the per-chunk (max, sum) of one row; chunk statistics are loaded 8 at a time
+// so their latencies overlap
 __device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS) {
-    float mm = -INFINITY;
-    for (int c = 0; c < NC; c++) mm = fmaxf(mm, st[c].x);
-    float S = 0.0f;
-    if (mm != -INFINITY)
-        for (int c = 0; c < NC; c++)
-            if (st[c].x != -INFINITY) S += st[c].y * __builtin_amdgcn_exp2f((st[c].x - mm) * kLog2e);
+    float mm = -INFINITY, S = 0.0f;
+    for (int c0 = 0; c0 < NC; c0 += 8) {
+        float2 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; k++) v[k] = c0 + k < NC ? st[c0 + k] : make_float2(-INFINITY, 0.0f);
+        float bm = mm;
+#pragma unroll
+        for (int k = 0; k < 8; k++) bm = fmaxf(bm, v[k].x);
+        if (bm != -INFINITY) {
+            float acc = S * __builtin_amdgcn_exp2f((mm - bm) * kLog2e);
+            if (mm == -INFINITY) acc = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 8; k++)
+                if (v[k].x != -INFINITY) acc += v[k].y * __builtin_amdgcn_exp2f((v[k].x - bm) * kLog2e);
+            S = acc;
+            mm = bm;
+        }
+    }
     m = mm;
     iS = S > 0.0f ? 1.0f / S : 0.0f;
 }
@@ -184,6 +206,7 @@ __global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
             pl.flag = 2;
             a.plan[i] = pl;
             a.accept_len[i] = 0;
+            if (a.flags) a.flags[i] = 2;
         }
         for (int t = lane; t < a.b; t += 64) a.out_tokens[(size_t)i * a.b + t] = -1;
         return;
@@ -237,21 +260,59 @@ __global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
     }
 }
 
-// weights of token v for a plan: (w_res, w_p) -- w_res is the residual (or bonus) weight,
-// w_p the fallback weight of P_a used when the residual is empty
+template <bool LOGITS>
+__device__ inline uint64_t weight_xy(const ReqPlan& pl, int col, float x, float y, float invT);
+
+// weight of token v in column col (see weight_xy), loading the values itself
 template <bool LOGITS, typename T>
-__device__ inline void weights_at(const AcceptArgs& a, const ReqPlan& pl, int v, uint64_t& wr, uint64_t& wp) {
-    const float pv = prob_of<LOGITS, T>(row_ptr<T>(a.target, pl.rowP, a.V), v, pl.mP, pl.iSP, a.invT);
-    if (pl.mode == 0) {
-        const float qv = prob_of<LOGITS, T>(row_ptr<T>(a.draft, pl.rowQ, a.V), v, pl.mQ, pl.iSQ, a.invT);
-        float r = pv - qv;
-        if (!(r > 0.0f)) r = 0.0f;
-        wr = weight_of(r);
-        wp = weight_of(pv);
-    } else {
-        wr = weight_of(pv);
-        wp = 0;
+__device__ inline uint64_t weight_at(const AcceptArgs& a, const ReqPlan& pl, int col, int v) {
+    const float x = load_x<T>(row_ptr<T>(a.target, pl.rowP, a.V), v);
+    const float y = (pl.mode == 0 && col == 0) ? load_x<T>(row_ptr<T>(a.draft, pl.rowQ, a.V), v) : x;
+    return weight_xy<LOGITS>(pl, col, x, y, a.invT);
+}
+
+// weight of one token from already loaded values x (target) and y (draft): column 0 is
+// the residual (or bonus) weight, column 1 the fallback weight of P_a
+template <bool LOGITS>
+__device__ inline uint64_t weight_xy(const ReqPlan& pl, int col, float x, float y, float invT) {
+    const float pv = LOGITS ? __builtin_amdgcn_exp2f((x * invT - pl.mP) * kLog2e) * pl.iSP : x;
+    if (pl.mode != 0 || col == 1) return weight_of(pv);
+    const float qv = LOGITS ? __builtin_amdgcn_exp2f((y * invT - pl.mQ) * kLog2e) * pl.iSQ : y;
+    float r = pv - qv;
+    if (!(r > 0.0f)) r = 0.0f;
+    return weight_of(r);
+}
+
+// Sum of one weight column over the contiguous range [lo, hi) of the vocabulary: 16-byte
+// loads when the range is aligned, element loads otherwise.
+template <bool LOGITS, typename T>
+__device__ inline uint64_t range_sum(const AcceptArgs& a, const ReqPlan& pl, int col, int lo, int hi) {
+    constexpr int VEC = 16 / sizeof(T);
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+    const T* prow = row_ptr<T>(a.target, pl.rowP, a.V);
+    const bool need_q = pl.mode == 0 && col == 0;
+    const T* qrow = need_q ? row_ptr<T>(a.draft, pl.rowQ, a.V) : prow;
+    uint64_t sum = 0;
+    int v = lo;
+    if ((a.V % VEC) == 0 && (lo % VEC) == 0) {
+        for (; v + VEC <= hi; v += VEC) {
+            const vec_t xp = *(const vec_t*)(prow + v);
+            vec_t xq = xp;
+            if (need_q) xq = *(const vec_t*)(qrow + v);
+#pragma unroll
+            for (int e = 0; e < VEC; e++) sum += weight_xy<LOGITS>(pl, col, to_f(xp[e]), to_f(xq[e]), a.invT);
+        }
     }
+    for (; v < hi; v++) sum += weight_xy<LOGITS>(pl, col, load_x<T>(prow, v), load_x<T>(qrow, v), a.invT);
+    return sum;
+}
+
+__device__ inline uint64_t wave_incl_scan_u64(uint64_t v, int lane) {
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t t = __shfl_up(v, off, 64);
+        if (lane >= off) v += t;
+    }
+    return v;
 }
 
 __device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
@@ -266,61 +327,56 @@ __device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
 }
 
 // ----------------------------------------------------------------------------------
-// ressum: grid (NCR, R)
+// chunk sums: grid (NCR, R); each workgroup sums the integer residual (or bonus) weights
+// of one vocabulary chunk of one request
 // ----------------------------------------------------------------------------------
 template <bool LOGITS, typename T>
-__global__ __launch_bounds__(kThreads) void ressum_kernel(AcceptArgs a) {
+__global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     __shared__ uint64_t red[kThreads / 64];
-    const int i = blockIdx.y, c = blockIdx.x;
+    const int i = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
     const ReqPlan pl = a.plan[i];
     if (pl.mode == 2) return;
+    const int per = (a.res_chunk + kThreads - 1) / kThreads;
     const int beg = c * a.res_chunk, end = min(a.V, beg + a.res_chunk);
-    uint64_t sr = 0, sp = 0;
-    for (int v = beg + threadIdx.x; v < end; v += kThreads) {
-        uint64_t wr, wp;
-        weights_at<LOGITS, T>(a, pl, v, wr, wp);
-        sr += wr;
-        sp += wp;
-    }
-    sr = block_sum_u64(sr, red);
-    sp = block_sum_u64(sp, red);
-    if (threadIdx.x == 0) {
-        a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
-        a.csum[((size_t)i * a.NCR + c) * 2 + 1] = sp;
-    }
+    const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
+    const uint64_t sr = block_sum_u64(range_sum<LOGITS, T>(a, pl, 0, lo, hi), red);
+    if (tid == 0) a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
 }
 
 // ----------------------------------------------------------------------------------
-// search: one workgroup per request
+// search: one workgroup per request. Z = sum of the chunk sums, the threshold
+// floor(m * Z / 2^24), the chunk holding it (wave scan), then the token inside that chunk
+// (per-thread ranges, block scan, and the owning thread's scan of its loaded values).
+// An empty residual falls back to the weights of P_a, summed here (rare).
 // ----------------------------------------------------------------------------------
 template <bool LOGITS, typename T>
 __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
     __shared__ uint64_t red[kThreads / 64];
-    __shared__ uint64_t scan[kThreads];
-    __shared__ int s_chunk;
+    __shared__ uint64_t wsum[kThreads / 64];
+    __shared__ int s_chunk, s_token;
     __shared__ uint64_t s_before;
-    __shared__ int s_token;
-    const int i = blockIdx.x, tid = threadIdx.x;
-    ReqPlan pl = a.plan[i];
-    if (pl.mode == 2) {
-        if (tid == 0 && a.flags) a.flags[i] = pl.flag;
-        return;
-    }
-    // Z of the residual and of the fallback
-    uint64_t zr = 0, zp = 0;
-    for (int c = tid; c < a.NCR; c += kThreads) {
-        zr += a.csum[((size_t)i * a.NCR + c) * 2 + 0];
-        zp += a.csum[((size_t)i * a.NCR + c) * 2 + 1];
-    }
-    zr = block_sum_u64(zr, red);
-    zp = block_sum_u64(zp, red);
+    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const ReqPlan pl = a.plan[i];
+    if (pl.mode == 2) return;
+    const int per = (a.res_chunk + kThreads - 1) / kThreads;
+    uint64_t Z = 0;
+    for (int k = tid; k < a.NCR; k += kThreads) Z += a.csum[((size_t)i * a.NCR + k) * 2 + 0];
+    Z = block_sum_u64(Z, red);
     int col = 0;
-    uint64_t Z = zr;
     int flag = pl.flag;
     if (Z == 0 && pl.mode == 0) {
         col = 1;
-        Z = zp;
         flag |= 1;
+        uint64_t zp = 0;
+        for (int k = 0; k < a.NCR; k++) {
+            const int beg = k * a.res_chunk, end = min(a.V, beg + a.res_chunk);
+            const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
+            const uint64_t sk = block_sum_u64(range_sum<LOGITS, T>(a, pl, 1, lo, hi), red);
+            if (tid == 0) a.csum[((size_t)i * a.NCR + k) * 2 + 1] = sk;
+            zp += sk;
+        }
+        __syncthreads();
+        Z = zp;
     }
     int token = -1;
     if (Z == 0) {
@@ -332,65 +388,79 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
         else if (u >= 1.0f) mu = (1u << 24) - 1;
         else mu = (uint32_t)(u * 16777216.0f);  // exact on the 2^-24 grid, truncates otherwise
         const uint64_t thr = (uint64_t)(((unsigned __int128)mu * Z) >> 24);
-        // 1. chunk holding thr: scan of chunk sums in rounds of kThreads chunks
-        if (tid == 0) s_chunk = -1;
-        uint64_t base = 0;
-        for (int c0 = 0; c0 < a.NCR; c0 += kThreads) {
-            const int c = c0 + tid;
-            const uint64_t v = c < a.NCR ? a.csum[((size_t)i * a.NCR + c) * 2 + col] : 0;
-            scan[tid] = v;
-            __syncthreads();
-            for (int off = 1; off < kThreads; off <<= 1) {  // Hillis-Steele inclusive scan
-                const uint64_t add = tid >= off ? scan[tid - off] : 0;
-                __syncthreads();
-                scan[tid] += add;
-                __syncthreads();
+        // 1. the chunk holding thr: wave 0 scans the chunk sums 64 at a time
+        if (w == 0) {
+            uint64_t base = 0, before = 0;
+            int found = -1;
+            for (int c0 = 0; c0 < a.NCR && found < 0; c0 += 64) {
+                const int k = c0 + lane;
+                const uint64_t v = k < a.NCR ? a.csum[((size_t)i * a.NCR + k) * 2 + col] : 0;
+                const uint64_t incl = base + wave_incl_scan_u64(v, lane);
+                const bool hit = k < a.NCR && v > 0 && incl - v <= thr && thr < incl;
+                const uint64_t m = __ballot(hit);
+                if (m) {
+                    const int src = __builtin_ctzll(m);
+                    found = c0 + src;
+                    before = __shfl(incl - v, src, 64);
+                }
+                base = __shfl(incl, 63, 64);
             }
-            const uint64_t incl = base + scan[tid];
-            const uint64_t excl = incl - v;
-            if (c < a.NCR && v > 0 && excl <= thr && thr < incl) {
-                s_chunk = c;
-                s_before = excl;
+            if (lane == 0) {
+                s_chunk = found;
+                s_before = before;
             }
-            base += scan[kThreads - 1];
-            __syncthreads();
-            if (s_chunk >= 0) break;
         }
-        const int c = s_chunk;
-        if (c >= 0) {
-            // 2. inside the chunk: contiguous per-thread ranges, exclusive scan, local search
-            const int beg = c * a.res_chunk, end = min(a.V, beg + a.res_chunk);
-            const int per = (a.res_chunk + kThreads - 1) / kThreads;
-            const int lo = beg + tid * per, hi = min(end, lo + per);
-            uint64_t loc = 0;
-            for (int v = lo; v < hi; v++) {
-                uint64_t wr, wp;
-                weights_at<LOGITS, T>(a, pl, v, wr, wp);
-                loc += col ? wp : wr;
-            }
-            scan[tid] = loc;
-            __syncthreads();
-            for (int off = 1; off < kThreads; off <<= 1) {
-                const uint64_t add = tid >= off ? scan[tid - off] : 0;
-                __syncthreads();
-                scan[tid] += add;
-                __syncthreads();
-            }
+        __syncthreads();
+        const int cs = s_chunk;
+        if (cs >= 0) {
+            // 2. inside the chunk: per-thread contiguous ranges, block exclusive scan
+            const int beg = cs * a.res_chunk, end = min(a.V, beg + a.res_chunk);
+            const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
+            const uint64_t loc = range_sum<LOGITS, T>(a, pl, col, lo, hi);
+            const uint64_t incl = wave_incl_scan_u64(loc, lane);
+            if (lane == 63) wsum[w] = incl;
             if (tid == 0) s_token = -1;
             __syncthreads();
+            uint64_t wbase = 0;
+            for (int k = 0; k < w; k++) wbase += wsum[k];
             const uint64_t rel = thr - s_before;
-            const uint64_t excl = scan[tid] - loc;
-            if (loc > 0 && excl <= rel && rel < scan[tid]) {
+            const uint64_t excl = wbase + incl - loc;
+            if (loc > 0 && excl <= rel && rel < excl + loc) {
+                // this thread's range holds the token: its values are loaded up front (no
+                // load waits inside the scan)
                 uint64_t cum = s_before + excl;
-                for (int v = lo; v < hi; v++) {
-                    uint64_t wr, wp;
-                    weights_at<LOGITS, T>(a, pl, v, wr, wp);
-                    const uint64_t wv = col ? wp : wr;
-                    if (cum + wv > thr) {
-                        s_token = v;
-                        break;
+                constexpr int VEC = 16 / sizeof(T);
+                typedef T vec_t __attribute__((ext_vector_type(VEC)));
+                constexpr int NV = (8192 / kThreads) / VEC;  // vectors per thread range
+                if (hi - lo == NV * VEC && (a.V % VEC) == 0 && (lo % VEC) == 0) {
+                    const T* prow = row_ptr<T>(a.target, pl.rowP, a.V) + lo;
+                    const bool need_q = pl.mode == 0 && col == 0;
+                    const T* qrow = need_q ? row_ptr<T>(a.draft, pl.rowQ, a.V) + lo : prow;
+                    vec_t xp[NV], xq[NV];
+#pragma unroll
+                    for (int k = 0; k < NV; k++) {
+                        xp[k] = ((const vec_t*)prow)[k];
+                        xq[k] = ((const vec_t*)qrow)[k];
                     }
-                    cum += wv;
+                    int found = -1;
+#pragma unroll
+                    for (int k = 0; k < NV; k++)
+#pragma unroll
+                        for (int e = 0; e < VEC; e++) {
+                            const uint64_t wv = weight_xy<LOGITS>(pl, col, to_f(xp[k][e]), to_f(xq[k][e]), a.invT);
+                            if (found < 0 && cum + wv > thr) found = lo + k * VEC + e;
+                            cum += wv;
+                        }
+                    s_token = found;
+                } else {
+                    for (int v = lo; v < hi; v++) {
+                        const uint64_t wv = weight_at<LOGITS, T>(a, pl, col, v);
+                        if (cum + wv > thr) {
+                            s_token = v;
+                            break;
+                        }
+                        cum += wv;
+                    }
                 }
             }
             __syncthreads();
@@ -465,10 +535,10 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-#define SV_ACCEPT_PHASES(LG, TT)                                                                    \
-    hipLaunchKernelGGL((decide_kernel<LG, TT>), dim3(d.num_reqs), dim3(64), 0, stream, a);          \
-    hipLaunchKernelGGL((ressum_kernel<LG, TT>), dim3(p.res_chunks, d.num_reqs), dim3(kThreads), 0, \
-                       stream, a);                                                                  \
+#define SV_ACCEPT_PHASES(LG, TT)                                                                      \
+    hipLaunchKernelGGL((decide_kernel<LG, TT>), dim3(d.num_reqs), dim3(64), 0, stream, a);            \
+    hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3(p.res_chunks, d.num_reqs), dim3(kThreads), 0, \
+                       stream, a);                                                                    \
     hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
     if (logits && bf) {
         SV_ACCEPT_PHASES(true, uint16_t);

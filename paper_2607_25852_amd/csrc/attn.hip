@@ -455,58 +455,61 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
 }
 
 
-// merge split partials: one wavefront per (row, head); lanes over d
+// merge split partials: grid (row chunk, kv-head, request), one thread per (query row of
+// the group, 4-dim slice); every split's lse and partial are loaded before any math (one
+// round of loads for up to 8 splits). Requests with a single split were written
+// directly by the main kernel and exit here.
 template <int HD, bool BF16OUT>
 __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
-    const int unit = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    const int K = a.qo[a.R];
-    if (K > a.total_q) return;
-    const int row = unit / a.Hq, head = unit % a.Hq;
-    if (row >= K) return;
-    // request of this row
-    int lo = 0, hi = a.R - 1;
-    while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (a.qo[mid] <= row) lo = mid; else hi = mid - 1;
-    }
-    const int i = lo;
+    constexpr int SL = HD / 4;  // 4-dim slices per row
+    const int h = blockIdx.y, i = blockIdx.z;
+    const int q0 = a.qo[i], k_i = a.qo[i + 1] - q0;
     int kv_len = a.kv_lens[i];
     if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
-    const int k_i = a.qo[i + 1] - a.qo[i];
-    if (kv_len - k_i < 0 || k_i > a.block) return;
+    if (k_i <= 0 || k_i > a.block || kv_len - k_i < 0 || q0 < 0 || q0 + k_i > a.total_q) return;
     const int nsplit = (kv_len + a.split - 1) / a.split;
     if (nsplit <= 1) return;
-    const size_t orow = (size_t)row * a.Hq + head;
+    const int u = blockIdx.x * 256 + threadIdx.x;
+    if (u >= a.G * k_i * SL) return;
+    const int r = u / SL, sl = u % SL;
+    const size_t orow = (size_t)(q0 + r / a.G) * a.Hq + h * a.G + r % a.G;
     const size_t sstride = (size_t)a.total_q * a.Hq;
-    float mx = -INFINITY;
-    for (int s = 0; s < nsplit; s++) mx = fmaxf(mx, a.part_lse[s * sstride + orow]);
-    constexpr int PER = HD / 64 > 0 ? HD / 64 : 1;
-    float acc[PER];
+    float mx = -INFINITY, wsum = 0.0f;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nsplit; s0 += 8) {
+        float lw[8];
+        f32x4 v[8];
 #pragma unroll
-    for (int e = 0; e < PER; e++) acc[e] = 0.0f;
-    float wsum = 0.0f;
-    for (int s = 0; s < nsplit; s++) {
-        const float l2 = a.part_lse[s * sstride + orow];
-        const float wgt = l2 == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(l2 - mx);
-        wsum += wgt;
-        const float* src = a.part_o + (s * sstride + orow) * HD;
-#pragma unroll
-        for (int e = 0; e < PER; e++) {
-            const int dd = lane + 64 * e;
-            if (dd < HD) acc[e] += wgt * src[dd];
+        for (int k = 0; k < 8; k++) {
+            const bool ok = s0 + k < nsplit;
+            lw[k] = ok ? a.part_lse[(s0 + k) * sstride + orow] : -INFINITY;
+            v[k] = ok ? *(const f32x4*)(a.part_o + ((s0 + k) * sstride + orow) * HD + sl * 4) : f32x4{0.f, 0.f, 0.f, 0.f};
         }
+        float bm = mx;
+#pragma unroll
+        for (int k = 0; k < 8; k++) bm = fmaxf(bm, lw[k]);
+        if (bm == -INFINITY) continue;
+        const float sc = mx == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(mx - bm);
+        wsum *= sc;
+        acc *= sc;
+#pragma unroll
+        for (int k = 0; k < 8; k++) {
+            const float wgt = lw[k] == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(lw[k] - bm);
+            wsum += wgt;
+            acc += wgt * v[k];
+        }
+        mx = bm;
     }
     const float inv = wsum > 0.0f ? 1.0f / wsum : 0.0f;
+    if (BF16OUT) {
+        uint64_t pk = 0;
 #pragma unroll
-    for (int e = 0; e < PER; e++) {
-        const int dd = lane + 64 * e;
-        if (dd < HD) {
-            if (BF16OUT) ((uint16_t*)a.out)[orow * HD + dd] = f2bf(acc[e] * inv);
-            else ((float*)a.out)[orow * HD + dd] = acc[e] * inv;
-        }
+        for (int e = 0; e < 4; e++) pk |= (uint64_t)f2bf(acc[e] * inv) << (16 * e);
+        *(uint64_t*)((uint16_t*)a.out + orow * HD + sl * 4) = pk;
+    } else {
+        *(f32x4*)((float*)a.out + orow * HD + sl * 4) = acc * inv;
     }
-    if (a.lse && lane == 0) a.lse[orow] = wsum > 0.0f ? (mx + __log2f(wsum)) * kLn2 : -INFINITY;
+    if (a.lse && sl == 0) a.lse[orow] = wsum > 0.0f ? (mx + __log2f(wsum)) * kLn2 : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------------
@@ -610,11 +613,12 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     }
     int split = d.kv_split;
     if (split <= 0) {
-        // at most ~16 splits for the longest request, 1024..8192 tokens each: enough work
-        // items to balance 256 CUs, few enough that the partial results stay small
-        long long want = ((long long)d.max_kv_len + 15) / 16;
-        if (want < 1024) want = 1024;
-        if (want > 8192) want = 8192;
+        // at most ~8 splits for the longest request, 4096..16384 tokens each: the
+        // persistent kernel balances the work items dynamically, and fewer splits keep
+        // the partial results (written, then merged) small
+        long long want = ((long long)d.max_kv_len + 7) / 8;
+        if (want < 4096) want = 4096;
+        if (want > 16384) want = 16384;
         split = (int)(((want + 63) / 64) * 64);
     }
     if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
@@ -703,11 +707,12 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
 #undef SV_LAUNCH_ATTN
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || plan.max_splits <= 1) return e;
-    const int units = d.total_q_max * d.num_q_heads;
+    const int rows_per_group = (d.num_q_heads / d.num_kv_heads) * d.block;
+    const dim3 mgrid((rows_per_group * (d.head_dim / 4) + 255) / 256, d.num_kv_heads, d.num_reqs);
     if (d.head_dim == 128)
-        hipLaunchKernelGGL((attn_merge_kernel<128, true>), dim3((units + 3) / 4), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((attn_merge_kernel<128, true>), mgrid, dim3(256), 0, stream, a);
     else
-        hipLaunchKernelGGL((attn_merge_kernel<64, true>), dim3((units + 3) / 4), dim3(256), 0, stream, a);
+        hipLaunchKernelGGL((attn_merge_kernel<64, true>), mgrid, dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -1,12 +1,12 @@
 // D-cut verification budget on one workgroup (AngelSpec Sec. 4.2).
 //
-// All R*b candidate positions fit in LDS (<= 8192). Each becomes a 64-bit key whose
-// order is the selection order: fp32 score bits in the high word (scores are >= +0,
-// so their bit patterns order like the values), then the depth inverted (shallower
-// first on equal scores), then the request index inverted (lower request first).
-// A bitonic sort in LDS ranks every key; the top K_j for every candidate ratio are
-// then prefixes of the sorted order, so utilities, the ratio choice and the keep
-// counts need no second selection.
+// All R*b candidate positions (<= 8192) become 64-bit keys whose order is the selection
+// order: fp32 score bits in the high word (scores are >= +0, so their bit patterns order
+// like the values), then the depth inverted (shallower first on equal scores), then the
+// request index inverted (lower request first). A bitonic sort ranks every key (held in
+// registers; only strides of 64 threads or more go through LDS); the top K_j of every
+// candidate ratio are then prefixes of the sorted order, so one prefix sum gives every
+// utility, and the keep counts need no second selection.
 #include "sv_internal.h"
 
 #pragma clang fp contract(off)
@@ -32,97 +32,142 @@ __device__ inline float clamp_conf(float c) {
 // floor(s * 2^40) for s in [0, 1]: exact (power-of-two scaling, fp64 holds it)
 __device__ inline uint64_t score_fixed(float s) { return (uint64_t)((double)s * 1099511627776.0); }
 
-__device__ inline uint64_t wave_sum_u64(uint64_t v) {
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
+// compare-exchange of a bitonic stage seen from element p holding x with partner value y
+// (partner index p ^ j); k is the size of the bitonic blocks being merged. The final
+// order is descending.
+__device__ inline uint64_t cmpx(uint64_t x, uint64_t y, int p, int j, int k) {
+    const bool desc = (p & k) == 0;
+    const bool lower = (p & j) == 0;
+    const bool keep_max = desc == lower;
+    return keep_max ? (x > y ? x : y) : (x < y ? x : y);
 }
 
+__device__ inline uint64_t shfl_xor_u64(uint64_t v, int m) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, m, 64);
+    const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), m, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
+    const uint32_t lo = __shfl_up((uint32_t)v, d, 64);
+    const uint32_t hi = __shfl_up((uint32_t)(v >> 32), d, 64);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// KPT keys per thread: thread t owns sorted positions t*KPT .. t*KPT+KPT-1. Bitonic
+// stages with stride < KPT run in registers, < 64*KPT across lanes of a wave, the
+// rest through LDS (ping-pong buffers, one barrier per stage).
+template <int KPT>
 __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const float* __restrict__ conf,
                                                           int32_t* __restrict__ keep,
                                                           int32_t* __restrict__ qo_indptr,
                                                           int32_t* __restrict__ sel,
                                                           float* __restrict__ scores_out,
                                                           uint64_t* __restrict__ util_out) {
-    __shared__ uint64_t keys[kMaxKeys];
+    constexpr int NPAD = KPT * kThreads;
+    __shared__ uint64_t lds[2][NPAD];
     __shared__ int cnt[kMaxReqs];
-    __shared__ uint64_t red[kThreads / 64][SV_MAX_RATIOS];
+    __shared__ uint64_t wtot[kThreads / 64];
+    __shared__ uint64_t s_util[SV_MAX_RATIOS];
     __shared__ int s_K;
     __shared__ int scan_tmp[kThreads / 64];
 
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int R = a.R, b = a.b, N = R * b;
-    int Npad = 2;
-    while (Npad < N) Npad <<= 1;
 
-    // 1. prefix scores, one request per thread, left to right in fp32 (eq. dcut-score)
+    // 1. prefix scores, one request per thread, left to right in fp32 (eq. dcut-score);
+    //    the confidences are first staged through LDS with coalesced loads (buffer 1 of
+    //    the key storage is free until the first LDS stage of the sort)
+    float* cst = (float*)&lds[1][0];
+    for (int e = tid; e < R * (b - 1); e += kThreads) cst[e] = conf[e];
+    __syncthreads();
     for (int i = tid; i < R; i += kThreads) {
         float s = 1.0f;
         for (int t = 0; t < b; t++) {
-            if (t > 0) s = s * clamp_conf(conf[(size_t)i * (b - 1) + (t - 1)]);
+            if (t > 0) s = s * clamp_conf(cst[i * (b - 1) + (t - 1)]);
             if (scores_out) scores_out[(size_t)i * b + t] = s;
-            keys[i * b + t] = ((uint64_t)__float_as_uint(s) << 32) |
-                              ((uint64_t)(0xFFFFu - (unsigned)t) << 16) | (uint64_t)(0xFFFFu - (unsigned)i);
+            lds[0][i * b + t] = ((uint64_t)__float_as_uint(s) << 32) |
+                                ((uint64_t)(0xFFFFu - (unsigned)t) << 16) | (uint64_t)(0xFFFFu - (unsigned)i);
         }
         cnt[i] = 0;
     }
-    for (int p = N + tid; p < Npad; p += kThreads) keys[p] = 0;  // below every real key
+    for (int p = N + tid; p < NPAD; p += kThreads) lds[0][p] = 0;  // below every real key
     __syncthreads();
+    uint64_t x[KPT];
+#pragma unroll
+    for (int e = 0; e < KPT; e++) x[e] = lds[0][tid * KPT + e];
 
-    // 2. bitonic sort, descending
-    for (int k = 2; k <= Npad; k <<= 1) {
+    // 2. bitonic sort, descending, of NPAD keys
+    int buf = 1;
+    for (int k = 2; k <= NPAD; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int p = tid; p < Npad; p += kThreads) {
-                const int q = p ^ j;
-                if (q > p) {
-                    const uint64_t x = keys[p], y = keys[q];
-                    const bool desc = (p & k) == 0;
-                    if (desc ? (x < y) : (x > y)) {
-                        keys[p] = y;
-                        keys[q] = x;
+            if (j < KPT) {
+#pragma unroll
+                for (int e = 0; e < KPT; e++) {
+                    const int p = tid * KPT + e;
+                    if ((e & j) == 0) {
+                        const uint64_t y0 = x[e], y1 = x[e | j];
+                        x[e] = cmpx(y0, y1, p, j, k);
+                        x[e | j] = cmpx(y1, y0, p | j, j, k);
                     }
                 }
+            } else if (j < 64 * KPT) {
+                const int m = j / KPT;
+#pragma unroll
+                for (int e = 0; e < KPT; e++) x[e] = cmpx(x[e], shfl_xor_u64(x[e], m), tid * KPT + e, j, k);
+            } else {
+#pragma unroll
+                for (int e = 0; e < KPT; e++) lds[buf][tid * KPT + e] = x[e];
+                __syncthreads();
+#pragma unroll
+                for (int e = 0; e < KPT; e++) {
+                    const int p = tid * KPT + e;
+                    x[e] = cmpx(x[e], lds[buf][p ^ j], p, j, k);
+                }
+                buf ^= 1;
             }
-            __syncthreads();
         }
     }
 
-    // 3. utilities of every ratio: sums over prefixes of the sorted order
-    const int nr = a.mode == SV_BUDGET_COST ? a.nratios : 1;
-    uint64_t u[SV_MAX_RATIOS];
-    for (int j = 0; j < SV_MAX_RATIOS; j++) u[j] = 0;
-    for (int p = tid; p < N; p += kThreads) {
-        const uint64_t f = score_fixed(__uint_as_float((uint32_t)(keys[p] >> 32)));
-        for (int j = 0; j < nr; j++) {
-            const int Kj = a.mode == SV_BUDGET_COST ? a.Kr[j] : a.fixed_K;
-            if (p < Kj) u[j] += f;
-        }
+    // 3. inclusive prefix sums of the fixed-point scores in sorted order; the utility of
+    //    budget K is the prefix at position K-1 (eq. dcut-batch-utility)
+    uint64_t f[KPT], run = 0;
+#pragma unroll
+    for (int e = 0; e < KPT; e++) {
+        run += score_fixed(__uint_as_float((uint32_t)(x[e] >> 32)));
+        f[e] = run;
     }
-    const int lane = tid & 63, wave = tid >> 6;
-    for (int j = 0; j < nr; j++) {
-        const uint64_t w = wave_sum_u64(u[j]);
-        if (lane == 0) red[wave][j] = w;
+    uint64_t incl = run;
+    for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t v = shfl_up_u64(incl, d);
+        if (lane >= d) incl += v;
+    }
+    if (lane == 63) wtot[wave] = incl;
+    __syncthreads();
+    uint64_t base = incl - run;
+    for (int w = 0; w < wave; w++) base += wtot[w];
+    const int nr = a.mode == SV_BUDGET_COST ? a.nratios : 1;
+    for (int jr = 0; jr < nr; jr++) {
+        const int Kj = a.mode == SV_BUDGET_COST ? a.Kr[jr] : a.fixed_K;
+        const int q = Kj - 1 - tid * KPT;
+        if (q >= 0 && q < KPT) s_util[jr] = base + f[q];
     }
     __syncthreads();
 
     // 4. ratio choice (eq. dcut-select), exact cross-multiplication, ties -> smaller ratio
     if (tid == 0) {
-        uint64_t U[SV_MAX_RATIOS];
-        for (int j = 0; j < nr; j++) {
-            uint64_t s = 0;
-            for (int w = 0; w < kThreads / 64; w++) s += red[w][j];
-            U[j] = s;
-            if (util_out) util_out[j] = s;
-        }
         int best = -1, K = a.fixed_K;
         if (a.mode == SV_BUDGET_COST) {
             best = 0;
-            for (int j = 1; j < nr; j++) {
-                const unsigned __int128 lhs = (unsigned __int128)U[j] * a.cost[best];
-                const unsigned __int128 rhs = (unsigned __int128)U[best] * a.cost[j];
-                if (lhs > rhs) best = j;
+            for (int jr = 1; jr < nr; jr++) {
+                const unsigned __int128 lhs = (unsigned __int128)s_util[jr] * a.cost[best];
+                const unsigned __int128 rhs = (unsigned __int128)s_util[best] * a.cost[jr];
+                if (lhs > rhs) best = jr;
             }
             K = a.Kr[best];
         }
+        if (util_out)
+            for (int jr = 0; jr < nr; jr++) util_out[jr] = s_util[jr];
         s_K = K;
         sel[0] = K;
         sel[1] = best;
@@ -131,32 +176,29 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
 
     // 5. kept positions per request: the first K keys of the sorted order
     const int K = s_K;
-    for (int p = tid; p < K; p += kThreads) {
-        const int i = 0xFFFF - (int)(keys[p] & 0xFFFFu);
-        atomicAdd(&cnt[i], 1);
-    }
+#pragma unroll
+    for (int e = 0; e < KPT; e++)
+        if (tid * KPT + e < K) atomicAdd(&cnt[0xFFFF - (int)(x[e] & 0xFFFFu)], 1);
     __syncthreads();
 
     // 6. keep = count - 1; qo_indptr = exclusive scan of the counts (block scan)
     constexpr int kPer = kMaxReqs / kThreads;  // 4 requests per thread
     int loc[kPer];
-    int run = 0;
+    int rsum = 0;
     for (int e = 0; e < kPer; e++) {
         const int i = tid * kPer + e;
         loc[e] = i < R ? cnt[i] : 0;
-        run += loc[e];
+        rsum += loc[e];
     }
-    // inclusive wave scan of run
-    int incl = run;
+    int iscan = rsum;
     for (int off = 1; off < 64; off <<= 1) {
-        const int v = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += v;
+        const int v = __shfl_up(iscan, off, 64);
+        if (lane >= off) iscan += v;
     }
-    if (lane == 63) scan_tmp[wave] = incl;
+    if (lane == 63) scan_tmp[wave] = iscan;
     __syncthreads();
-    int base = 0;
-    for (int w = 0; w < wave; w++) base += scan_tmp[w];
-    int pos = base + incl - run;
+    int pos = iscan - rsum;
+    for (int w = 0; w < wave; w++) pos += scan_tmp[w];
     for (int e = 0; e < kPer; e++) {
         const int i = tid * kPer + e;
         if (i < R) {
@@ -188,8 +230,14 @@ hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* ke
         a.Kr[j] = (int)Kj;
         a.cost[j] = d.cost[j];
     }
-    hipLaunchKernelGGL(budget_kernel, dim3(1), dim3(kThreads), 0, stream, a, conf, keep, qo_indptr, sel,
-                       scores, utility);
+    const int64_t kpt = (N + kThreads - 1) / kThreads;
+#define SV_LAUNCH_BUDGET(KP) \
+    hipLaunchKernelGGL(budget_kernel<KP>, dim3(1), dim3(kThreads), 0, stream, a, conf, keep, qo_indptr, sel, scores, utility)
+    if (kpt <= 1) SV_LAUNCH_BUDGET(1);
+    else if (kpt <= 2) SV_LAUNCH_BUDGET(2);
+    else if (kpt <= 4) SV_LAUNCH_BUDGET(4);
+    else SV_LAUNCH_BUDGET(8);
+#undef SV_LAUNCH_BUDGET
     return hipGetLastError();
 }
 
