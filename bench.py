@@ -23,10 +23,141 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+ATTN_SRC = os.path.join(ROOT, "paper_2607_25852_amd", "csrc", "attn.hip")
+# HBM traffic of one sv_verify_attn call, from rocprofv3 FETCH_SIZE / WRITE_SIZE runs
+# scaled by a copy kernel of known size; valid only while the attention source is the
+# one that was measured (its digest is recorded beside the figure)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sv_verify_attn_c64_b16_traffic.md")
+COPY_BYTES = 1 << 30  # copy-probe size: 1 GiB read + 1 GiB written, well above the 256 MB MALL
+ATTN_KERNELS = ("attn_plan_kernel", "attn_bf16_kernel", "attn_merge_kernel")
 
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def attn_source_digest():
+    import hashlib
+    with open(ATTN_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def recorded_traffic(workload):
+    """Bytes per call recorded for this workload and the current attention source, else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_FILE):
+        line = line.strip().lstrip("-").strip()
+        if ":" in line:
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    if fields.get("workload") != workload or fields.get("attn_source_sha256") != attn_source_digest():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_call"])
+    except (KeyError, ValueError):
+        return None
+
+
+def short_name(name):
+    n = name.replace("void ", "").replace("sv::(anonymous namespace)::", "")
+    depth = 0
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            n = n[:i]
+            break
+    return n if len(n) <= 90 else n[:87] + "..."
+
+
+def summarize_trace(stats_csv):
+    """Markdown table of a rocprofv3 --stats kernel summary (run_kernel_stats.csv)."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    out = ["| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| `{short_name(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                   f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | {float(r['Percentage']):.1f}% |")
+    attn = [r for r in rows if any(k in r["Name"] for k in ATTN_KERNELS)]
+    if attn:
+        calls = max(int(r["Calls"]) for r in attn if "attn_bf16_kernel" in r["Name"]) if any(
+            "attn_bf16_kernel" in r["Name"] for r in attn) else 1
+        tot = sum(float(r["TotalDurationNs"]) for r in attn) / calls / 1e3
+        out.append("")
+        out.append(f"sv_verify_attn kernels per call (plan + attention + merge): {tot:.1f} us")
+    return "\n".join(out)
+
+
+def summarize_traffic(fetch_dir, write_dir):
+    """FETCH_SIZE / WRITE_SIZE per dispatch, scaled by the copy probe, as traffic per call."""
+    import csv
+    import collections
+
+    def per_kernel(d, counter):
+        vals = collections.defaultdict(list)
+        for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))):
+            if r["Counter_Name"] == counter:
+                vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+        return vals
+
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+
+    def pick(vals, key):
+        return {k: v for k, v in vals.items() if key in k}
+
+    cf, cw = pick(fetch, "neg_kernel"), pick(write, "neg_kernel")
+    assert cf and cw, "copy probe kernel not found in the counter runs"
+    copy_fetch_kib = sum(sum(v) for v in cf.values()) / sum(len(v) for v in cf.values())
+    copy_write_kib = sum(sum(v) for v in cw.values()) / sum(len(v) for v in cw.values())
+    f_fetch = COPY_BYTES / (copy_fetch_kib * 1024)
+    f_write = COPY_BYTES / (copy_write_kib * 1024)
+    out = ["| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |", "|---|---|---|---|"]
+    for k in sorted(set(fetch) | set(write)):
+        if not (any(a in k for a in ATTN_KERNELS) or "neg_kernel" in k):
+            continue
+        fv, wv = fetch.get(k, [0.0]), write.get(k, [0.0])
+        out.append(f"| `{short_name(k)}` | {len(fv)} | {sum(fv) / len(fv):.0f} | {sum(wv) / len(wv):.0f} |")
+    main_calls = sum(len(v) for k, v in fetch.items() if "attn_bf16_kernel" in k)
+    tf = sum(sum(v) for k, v in fetch.items() if any(a in k for a in ATTN_KERNELS)) / main_calls
+    tw = sum(sum(v) for k, v in write.items() if any(a in k for a in ATTN_KERNELS)) / main_calls
+    traffic = tf * 1024 * f_fetch + tw * 1024 * f_write
+    bench = {}
+    bj = os.path.join(fetch_dir, "bench.json")
+    if os.path.exists(bj):
+        lines = [l for l in open(bj) if l.startswith("{")]
+        if lines:
+            bench = json.loads(lines[-1])
+    alg = bench.get("roofline", {}).get("algorithmic_bytes")
+    out += ["",
+            f"- copy probe: {COPY_BYTES} bytes read and written; FETCH_SIZE {copy_fetch_kib:.0f} KiB, "
+            f"WRITE_SIZE {copy_write_kib:.0f} KiB; scale factors fetch {f_fetch:.4f}, write {f_write:.4f}",
+            f"- calls: {main_calls}",
+            f"- fetch_bytes_per_call: {tf * 1024 * f_fetch:.0f}",
+            f"- write_bytes_per_call: {tw * 1024 * f_write:.0f}",
+            f"- traffic_bytes_per_call: {traffic:.0f}"]
+    if alg:
+        out.append(f"- algorithmic_bytes_per_call: {alg:.0f} (traffic / algorithmic = {traffic / alg:.3f})")
+    out.append(f"- workload: {bench.get('config', {}).get('workload', '?').split(':')[0]}")
+    # the digest of the source that ran (recorded by the bench run itself)
+    out.append(f"- attn_source_sha256: {bench.get('roofline', {}).get('attn_source_sha256', '?')}")
+    return "\n".join(out)
+
+
+def copy_probe():
+    """A plain elementwise copy (y = -x, fp32) of COPY_BYTES, three times: calibrates
+    the FETCH_SIZE / WRITE_SIZE counters against a known byte count."""
+    import torch
+    src = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda").uniform_()
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def attn_bytes(cfg, L, k):
@@ -86,7 +217,17 @@ def main():
     ap.add_argument("--workload", default="c64_b16")
     ap.add_argument("--kv-split", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="host time for the oracle baseline (0: skip)")
+    ap.add_argument("--copy-probe", action="store_true", help="also run a 1 GiB copy kernel (counter calibration)")
+    ap.add_argument("--summarize-trace", metavar="CSV", help="print a rocprofv3 kernel-stats CSV as markdown")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="print HBM traffic per sv_verify_attn call from two rocprofv3 --pmc runs")
     args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
+    if args.summarize_traffic:
+        print(summarize_traffic(*args.summarize_traffic))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the round's kernels run on a single MI355X and this build "
               "has no multi-GPU path (see the sharding note in DESIGN.md); run with --gpus 1.", file=sys.stderr)
@@ -142,6 +283,11 @@ def main():
     log(f"step {ms_step:.3f} ms: budget {t_budget * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us "
         f"({a_gbs:.0f} GB/s), acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
 
+    if args.copy_probe:
+        log("copy probe")
+        copy_probe()
+    traffic = recorded_traffic(cfg.name) if args.kv_split == 0 else None
+
     cpu = None
     if args.cpu_seconds > 0:
         log("timing the oracle on the host")
@@ -166,9 +312,10 @@ def main():
                    "concurrency": cfg.R, "block": cfg.b, "verified_positions": int(rnd.K),
                    "verified_drafts": drafts, "budget_ratio_index": int(rnd.sel[1].item()),
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (split-KV attention + partial merge)",
+        "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (plan + split-KV attention + partial merge)",
                      "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
-                     "traffic": None, "algorithmic_bytes": a_bytes},
+                     "traffic": traffic, "traffic_unit": "HBM bytes per call", "algorithmic_bytes": a_bytes,
+                     "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest()},
         "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
                     "acceptance_algorithmic_bytes": x_bytes},

@@ -23,6 +23,9 @@
  *     only enqueues kernels on `stream` (a hipStream_t; NULL = the default
  *     stream) and returns without waiting for them.
  *   - Descriptors are host structs, read during the call only.
+ *   - Alignment: the floating-point data arrays (q, caches, out, logits) and the
+ *     workspaces must be 16-byte aligned; int32 and fp32 index / scalar arrays
+ *     4-byte aligned. Misaligned pointers are rejected with SV_ERR_INVALID_ARG.
  *   - Host-side argument checks run before anything is enqueued. On failure the
  *     call returns a non-zero sv_status, enqueues nothing, and sv_last_error()
  *     (thread-local) describes the reason. A failed launch returns SV_ERR_HIP.

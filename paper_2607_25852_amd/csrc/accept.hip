@@ -26,6 +26,8 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kThreads = 256;
 constexpr int kStatsLoads = 8;  // 16-byte loads in flight per thread in rowstats
+constexpr int kResChunk = 8192;  // vocabulary chunk of the residual sums
+constexpr int kResPer = kResChunk / kThreads;  // tokens per thread in a chunk
 
 struct ReqPlan {
     int a, n, mode, flag;  // mode 0: residual after a rejection, 1: bonus, 2: nothing to draw
@@ -71,18 +73,17 @@ __device__ inline float prob_of(const T* row, int v, float m, float iS, float in
     }
 }
 
-// floor(min(r, 1) * 2^40) for r > 0 (0 for r <= 0 or NaN), from the fp32 bits: a normal
-// r is m * 2^(e - 150) with m the 24-bit significand and e the biased exponent, so
-// r * 2^40 = m * 2^(e - 110); subnormals give less than 2^-86, i.e. 0.
+// floor(min(r, 1) * 2^40) for r > 0 (0 for r <= 0 or NaN). v = min(r, 1) * 2^40 is exact
+// (a power-of-two scaling) and below 2^41; its multiple of 2^32 (hi) and the remainder
+// (lo = v - hi * 2^32, exact: both are multiples of the unit in the last place of v) are
+// truncated to integers by the hardware conversion, so the result is floor(v) exactly.
 __device__ inline uint64_t weight_of(float r) {
-    if (!(r > 0.0f)) return 0;
-    if (r >= 1.0f) return 1ull << 40;
-    const uint32_t u = __float_as_uint(r);
-    const int e = (int)(u >> 23);
-    if (e == 0) return 0;
-    const uint64_t m = (uint64_t)((u & 0x7FFFFFu) | 0x800000u);
-    const int sh = e - 110;  // <= 16 because r < 1
-    return sh >= 0 ? (m << sh) : (sh > -64 ? (m >> -sh) : 0);
+    r = r > 0.0f ? r : 0.0f;
+    r = r < 1.0f ? r : 1.0f;
+    const float v = r * 1099511627776.0f;                          // 2^40
+    const float hf = __builtin_truncf(v * 2.3283064365386963e-10f);  // floor(v / 2^32)
+    const float lf = v - hf * 4294967296.0f;
+    return ((uint64_t)(uint32_t)hf << 32) | (uint64_t)(uint32_t)lf;
 }
 
 template <typename T>
@@ -307,6 +308,46 @@ __device__ inline uint64_t range_sum(const AcceptArgs& a, const ReqPlan& pl, int
     return sum;
 }
 
+// One thread's full, aligned range of kResPer tokens: every load is issued before any
+// weight is computed (one memory round trip), and the values stay in registers for a
+// later scan.
+template <typename T>
+struct RangeRegs {
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int NV = kResPer / VEC;
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+    vec_t xp[NV], xq[NV];
+};
+
+template <typename T>
+__device__ inline bool range_is_full(const AcceptArgs& a, int lo, int hi) {
+    return hi - lo == kResPer && (a.V % RangeRegs<T>::VEC) == 0 && (lo % RangeRegs<T>::VEC) == 0;
+}
+
+template <typename T>
+__device__ inline void range_load(const AcceptArgs& a, const ReqPlan& pl, int col, int lo, RangeRegs<T>& g) {
+    typedef typename RangeRegs<T>::vec_t vec_t;
+    const vec_t* prow = (const vec_t*)(row_ptr<T>(a.target, pl.rowP, a.V) + lo);
+    const bool need_q = pl.mode == 0 && col == 0;
+    const vec_t* qrow = need_q ? (const vec_t*)(row_ptr<T>(a.draft, pl.rowQ, a.V) + lo) : prow;
+#pragma unroll
+    for (int k = 0; k < RangeRegs<T>::NV; k++) {
+        g.xp[k] = prow[k];
+        g.xq[k] = qrow[k];
+    }
+}
+
+template <bool LOGITS, typename T>
+__device__ inline uint64_t range_regs_sum(const AcceptArgs& a, const ReqPlan& pl, int col, const RangeRegs<T>& g) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < RangeRegs<T>::NV; k++)
+#pragma unroll
+        for (int e = 0; e < RangeRegs<T>::VEC; e++)
+            sum += weight_xy<LOGITS>(pl, col, to_f(g.xp[k][e]), to_f(g.xq[k][e]), a.invT);
+    return sum;
+}
+
 __device__ inline uint64_t wave_incl_scan_u64(uint64_t v, int lane) {
     for (int off = 1; off < 64; off <<= 1) {
         const uint64_t t = __shfl_up(v, off, 64);
@@ -336,10 +377,17 @@ __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     const int i = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
     const ReqPlan pl = a.plan[i];
     if (pl.mode == 2) return;
-    const int per = (a.res_chunk + kThreads - 1) / kThreads;
-    const int beg = c * a.res_chunk, end = min(a.V, beg + a.res_chunk);
-    const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
-    const uint64_t sr = block_sum_u64(range_sum<LOGITS, T>(a, pl, 0, lo, hi), red);
+    const int beg = c * kResChunk, end = min(a.V, beg + kResChunk);
+    const int lo = min(end, beg + tid * kResPer), hi = min(end, lo + kResPer);
+    uint64_t part;
+    if (range_is_full<T>(a, lo, hi)) {
+        RangeRegs<T> g;
+        range_load<T>(a, pl, 0, lo, g);
+        part = range_regs_sum<LOGITS, T>(a, pl, 0, g);
+    } else {
+        part = range_sum<LOGITS, T>(a, pl, 0, lo, hi);
+    }
+    const uint64_t sr = block_sum_u64(part, red);
     if (tid == 0) a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
 }
 
@@ -358,9 +406,15 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
     const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const ReqPlan pl = a.plan[i];
     if (pl.mode == 2) return;
-    const int per = (a.res_chunk + kThreads - 1) / kThreads;
-    uint64_t Z = 0;
-    for (int k = tid; k < a.NCR; k += kThreads) Z += a.csum[((size_t)i * a.NCR + k) * 2 + 0];
+    const int per = kResPer;
+    // chunk sums: thread k < NCR keeps csum[k] in a register (wave 0 scans them below when
+    // there are at most 64 chunks)
+    uint64_t Z = 0, my_cs = 0;
+    for (int k = tid; k < a.NCR; k += kThreads) {
+        const uint64_t v = a.csum[((size_t)i * a.NCR + k) * 2 + 0];
+        if (k == tid) my_cs = v;
+        Z += v;
+    }
     Z = block_sum_u64(Z, red);
     int col = 0;
     int flag = pl.flag;
@@ -394,7 +448,8 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
             int found = -1;
             for (int c0 = 0; c0 < a.NCR && found < 0; c0 += 64) {
                 const int k = c0 + lane;
-                const uint64_t v = k < a.NCR ? a.csum[((size_t)i * a.NCR + k) * 2 + col] : 0;
+                const uint64_t v = k >= a.NCR ? 0 : (col == 0 && a.NCR <= 64) ? my_cs
+                                                             : a.csum[((size_t)i * a.NCR + k) * 2 + col];
                 const uint64_t incl = base + wave_incl_scan_u64(v, lane);
                 const bool hit = k < a.NCR && v > 0 && incl - v <= thr && thr < incl;
                 const uint64_t m = __ballot(hit);
@@ -414,9 +469,17 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
         const int cs = s_chunk;
         if (cs >= 0) {
             // 2. inside the chunk: per-thread contiguous ranges, block exclusive scan
-            const int beg = cs * a.res_chunk, end = min(a.V, beg + a.res_chunk);
+            const int beg = cs * kResChunk, end = min(a.V, beg + kResChunk);
             const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
-            const uint64_t loc = range_sum<LOGITS, T>(a, pl, col, lo, hi);
+            const bool full = range_is_full<T>(a, lo, hi);
+            RangeRegs<T> g;
+            uint64_t loc;
+            if (full) {
+                range_load<T>(a, pl, col, lo, g);
+                loc = range_regs_sum<LOGITS, T>(a, pl, col, g);
+            } else {
+                loc = range_sum<LOGITS, T>(a, pl, col, lo, hi);
+            }
             const uint64_t incl = wave_incl_scan_u64(loc, lane);
             if (lane == 63) wsum[w] = incl;
             if (tid == 0) s_token = -1;
@@ -426,29 +489,17 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
             const uint64_t rel = thr - s_before;
             const uint64_t excl = wbase + incl - loc;
             if (loc > 0 && excl <= rel && rel < excl + loc) {
-                // this thread's range holds the token: its values are loaded up front (no
-                // load waits inside the scan)
+                // this thread's range holds the token; a full range scans the values it
+                // already holds
                 uint64_t cum = s_before + excl;
-                constexpr int VEC = 16 / sizeof(T);
-                typedef T vec_t __attribute__((ext_vector_type(VEC)));
-                constexpr int NV = (8192 / kThreads) / VEC;  // vectors per thread range
-                if (hi - lo == NV * VEC && (a.V % VEC) == 0 && (lo % VEC) == 0) {
-                    const T* prow = row_ptr<T>(a.target, pl.rowP, a.V) + lo;
-                    const bool need_q = pl.mode == 0 && col == 0;
-                    const T* qrow = need_q ? row_ptr<T>(a.draft, pl.rowQ, a.V) + lo : prow;
-                    vec_t xp[NV], xq[NV];
-#pragma unroll
-                    for (int k = 0; k < NV; k++) {
-                        xp[k] = ((const vec_t*)prow)[k];
-                        xq[k] = ((const vec_t*)qrow)[k];
-                    }
+                if (full) {
                     int found = -1;
 #pragma unroll
-                    for (int k = 0; k < NV; k++)
+                    for (int k = 0; k < RangeRegs<T>::NV; k++)
 #pragma unroll
-                        for (int e = 0; e < VEC; e++) {
-                            const uint64_t wv = weight_xy<LOGITS>(pl, col, to_f(xp[k][e]), to_f(xq[k][e]), a.invT);
-                            if (found < 0 && cum + wv > thr) found = lo + k * VEC + e;
+                        for (int e = 0; e < RangeRegs<T>::VEC; e++) {
+                            const uint64_t wv = weight_xy<LOGITS>(pl, col, to_f(g.xp[k][e]), to_f(g.xq[k][e]), a.invT);
+                            if (found < 0 && cum + wv > thr) found = lo + k * RangeRegs<T>::VEC + e;
                             cum += wv;
                         }
                     s_token = found;
@@ -481,7 +532,7 @@ AcceptPlan plan_accept(const sv_accept_desc& d) {
     const int vec = 16 / esz;
     p.stats_chunk = kThreads * kStatsLoads * vec;  // 32 KB of logits per workgroup
     p.stats_chunks = (d.vocab + p.stats_chunk - 1) / p.stats_chunk;
-    p.res_chunk = 8192;
+    p.res_chunk = kResChunk;
     p.res_chunks = (d.vocab + p.res_chunk - 1) / p.res_chunk;
     const size_t R = d.num_reqs, b = d.block, D = b > 1 ? b - 1 : 1;
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };

@@ -393,43 +393,77 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     }
 }
 
-// Plan of the persistent attention kernel: one entry (request << 16 | split) per split
-// of every valid request, the number of work items (entries x kv-heads x row blocks) and
-// a zeroed work counter. One workgroup; requests are scanned in chunks.
+// Work list, largest items first. Every (request, split) group is bucketed by its tile
+// count: full splits share the top bucket, a request's shorter last split lands in the
+// bucket of its own length. The buckets are laid out in decreasing size (a counting
+// sort), so the persistent workgroups take the long items early and the short ones fill
+// the tail. The order inside a bucket is unspecified and does not affect any result:
+// every item writes its own output rows or partial slot.
+__device__ inline int plan_splits(const AttnArgs& a, int i, int& last_tiles) {
+    const int q0 = a.qo[i], k_i = a.qo[i + 1] - q0;
+    int kv_len = a.kv_lens[i];
+    if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
+    last_tiles = 0;
+    if (!(k_i >= 1 && k_i <= a.block && kv_len - k_i >= 0 && q0 >= 0 && q0 + k_i <= a.total_q)) return 0;
+    const int ns = (kv_len + a.split - 1) / a.split;
+    last_tiles = (kv_len - (ns - 1) * a.split + kTile - 1) / kTile;
+    return ns;
+}
+
 __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnArgs a, int32_t* groups, int32_t* ctr) {
+    constexpr int NB = 1024;  // size buckets (tile counts 1..NB; longer splits share the last)
+    __shared__ int cursor[NB];
     __shared__ int wsum[16];
-    __shared__ int carry;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    if (tid == 0) carry = 0;
+    const int full_tiles = a.split / kTile;
+    auto bucket = [](int tiles) { return tiles < NB ? tiles - 1 : NB - 1; };
+    const int fb = bucket(full_tiles);
+    cursor[tid] = 0;
     __syncthreads();
+    // 1. histogram of group sizes (full splits summed per wave first: one shared bucket)
     for (int base = 0; base < a.R; base += 1024) {
         const int i = base + tid;
-        int ns = 0;
-        if (i < a.R) {
-            const int q0 = a.qo[i], k_i = a.qo[i + 1] - q0;
-            int kv_len = a.kv_lens[i];
-            if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
-            if (k_i >= 1 && k_i <= a.block && kv_len - k_i >= 0 && q0 >= 0 && q0 + k_i <= a.total_q)
-                ns = (kv_len + a.split - 1) / a.split;
-        }
-        int incl = ns;
-        for (int off = 1; off < 64; off <<= 1) {
-            const int v = __shfl_up(incl, off, 64);
-            if (lane >= off) incl += v;
-        }
-        if (lane == 63) wsum[w] = incl;
-        __syncthreads();
-        int pre = carry;
-        for (int k = 0; k < w; k++) pre += wsum[k];
-        const int start = pre + incl - ns;
-        for (int t = 0; t < ns; t++) groups[start + t] = (i << 16) | t;
-        __syncthreads();
-        if (tid == 1023) carry = start + ns;
-        __syncthreads();
+        int last = 0, ns = i < a.R ? plan_splits(a, i, last) : 0;
+        int full = ns > 1 ? ns - 1 : 0;
+        for (int off = 32; off > 0; off >>= 1) full += __shfl_xor(full, off, 64);
+        if (lane == 0 && full) atomicAdd(&cursor[fb], full);
+        if (ns > 0) atomicAdd(&cursor[bucket(last)], 1);
     }
-    if (tid == 0) {
-        ctr[0] = carry * a.Hkv * a.nrb;
+    __syncthreads();
+    // 2. bucket starts in decreasing size: thread t scans bucket NB-1-t
+    const int bk = NB - 1 - tid;
+    const int cnt = cursor[bk];
+    int incl = cnt;
+    for (int off = 1; off < 64; off <<= 1) {
+        const int v = __shfl_up(incl, off, 64);
+        if (lane >= off) incl += v;
+    }
+    if (lane == 63) wsum[w] = incl;
+    __syncthreads();
+    int pre = 0;
+    for (int k = 0; k < w; k++) pre += wsum[k];
+    cursor[bk] = pre + incl - cnt;
+    if (tid == 1023) {
+        ctr[0] = (pre + incl) * a.Hkv * a.nrb;
         ctr[1] = 0;
+    }
+    __syncthreads();
+    // 3. place the groups (full splits: one atomic per wave, positions by a wave scan)
+    for (int base = 0; base < a.R; base += 1024) {
+        const int i = base + tid;
+        int last = 0, ns = i < a.R ? plan_splits(a, i, last) : 0;
+        const int full = ns > 1 ? ns - 1 : 0;
+        int fincl = full;
+        for (int off = 1; off < 64; off <<= 1) {
+            const int v = __shfl_up(fincl, off, 64);
+            if (lane >= off) fincl += v;
+        }
+        int fbase = 0;
+        if (lane == 63 && fincl) fbase = atomicAdd(&cursor[fb], fincl);
+        fbase = __shfl(fbase, 63, 64);
+        const int p0 = fbase + fincl - full;
+        for (int t = 0; t < full; t++) groups[p0 + t] = (int32_t)(((uint32_t)i << 16) | (uint32_t)t);
+        if (ns > 0) groups[atomicAdd(&cursor[bucket(last)], 1)] = (int32_t)(((uint32_t)i << 16) | (uint32_t)(ns - 1));
     }
 }
 
@@ -448,9 +482,9 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
         const int item = s_item;
         __syncthreads();
         if (item >= nitems) break;
-        const int gv = groups[item / per_group];
+        const uint32_t gv = (uint32_t)groups[item / per_group];  // request << 16 | split
         const int within = item % per_group;
-        attn_item<HD, NW, NBUF, ONEPAGE>(a, lds, gv >> 16, within / a.nrb, gv & 0xFFFF, within % a.nrb);
+        attn_item<HD, NW, NBUF, ONEPAGE>(a, lds, (int)(gv >> 16), within / a.nrb, (int)(gv & 0xFFFFu), within % a.nrb);
     }
 }
 

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <cstdint>
 
 #include "sv_internal.h"
 
@@ -36,6 +37,10 @@ sv_status launched(hipError_t e, const char* what) {
 
 bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// every pointer must be NULL or aligned to `a` bytes (16 for the arrays read with 16-byte
+// vector loads or LDS DMA, 4 for the int32 / fp32 arrays)
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
 sv_status check_budget(const sv_budget_desc* d, const float* conf, const int32_t* keep,
                        const int32_t* qo, const int32_t* sel) {
     if (!d) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: desc is NULL");
@@ -48,6 +53,8 @@ sv_status check_budget(const sv_budget_desc* d, const float* conf, const int32_t
         return fail(SV_ERR_UNSUPPORTED, "sv_alloc_budget: num_reqs*block = %lld above %d", N, SV_MAX_BUDGET_POSITIONS);
     if (!keep || !qo || !sel) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: keep/qo_indptr/sel must not be NULL");
     if (d->block > 1 && !conf) return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: conf is NULL");
+    if (!aligned(conf, 4) || !aligned(keep, 4) || !aligned(qo, 4) || !aligned(sel, 4))
+        return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: arrays must be 4-byte aligned");
     if (d->mode == SV_BUDGET_FIXED) {
         if (d->fixed_budget < d->num_reqs || d->fixed_budget > N)
             return fail(SV_ERR_INVALID_ARG, "sv_alloc_budget: fixed_budget %d outside [R=%d, R*b=%lld]",
@@ -156,6 +163,10 @@ sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_
     if (st != SV_OK) return st;
     if (!q || !k_cache || !v_cache || !page_table || !qo_indptr || !kv_lens || !out)
         return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: a required pointer is NULL");
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) || !aligned(ws, 16) ||
+        !aligned(page_table, 4) || !aligned(qo_indptr, 4) || !aligned(kv_lens, 4) || !aligned(lse, 4))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_verify_attn: q, caches, out and ws must be 16-byte aligned, int32/fp32 arrays 4-byte aligned");
     const sv::AttnPlan p = sv::plan_attn(*desc);
     const size_t need = p.ws_bytes;
     if (need && (!ws || ws_bytes < need))
@@ -183,6 +194,11 @@ sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const v
     if (!target || !qo_indptr || !u_sample || !accept_len || !out_tokens ||
         (has_drafts && (!draft || !draft_tokens || !u_accept)))
         return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: a required pointer is NULL");
+    if (!aligned(target, 16) || !aligned(draft, 16) || !aligned(ws, 16) || !aligned(draft_tokens, 4) ||
+        !aligned(qo_indptr, 4) || !aligned(u_accept, 4) || !aligned(u_sample, 4) || !aligned(accept_len, 4) ||
+        !aligned(out_tokens, 4) || !aligned(flags, 4))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_spec_accept: target, draft and ws must be 16-byte aligned, int32/fp32 arrays 4-byte aligned");
     const sv::AcceptPlan p = sv::plan_accept(*desc);
     if (!ws || ws_bytes < p.total)
         return fail(SV_ERR_WORKSPACE, "sv_spec_accept: workspace of %zu bytes needed, %zu given", p.total,

@@ -164,3 +164,24 @@ def test_injected_launch_failure_enqueues_nothing(lib, monkeypatch):
     st = lib.sv_spec_accept(ctypes.byref(d), fake, fake, fake, fake, fake, fake, fake, fake, None, fake, need - 1,
                             None)
     assert st == B.SV_ERR_WORKSPACE
+
+
+def test_misaligned_pointers_are_rejected(lib):
+    """Checked on the host before any launch (the fake addresses are never touched)."""
+    ok16, odd = ctypes.c_void_p(4096), ctypes.c_void_p(4096 + 2)
+    d = B.budget_desc(4, 8, "fixed", fixed_budget=32)
+    st = lib.sv_alloc_budget(ctypes.byref(d), odd, ok16, ok16, ok16, None, None, None)
+    assert st == B.SV_ERR_INVALID_ARG and "aligned" in B.last_error()
+    d = B.attn_desc(4, 64, 16, 32, 8, 128, 64, 130, 1000, 8200, B.SV_BF16)
+    need = lib.sv_verify_attn_workspace_size(ctypes.byref(d))
+    args = [ok16] * 7
+    for bad in range(7):
+        a = list(args)
+        a[bad] = ctypes.c_void_p(4096 + (8 if bad in (0, 1, 2, 6) else 2))
+        st = lib.sv_verify_attn(ctypes.byref(d), *a, ok16, ok16, need, None)
+        assert st == B.SV_ERR_INVALID_ARG and "aligned" in B.last_error(), bad
+    d = B.accept_desc(4, 8, 1024, B.SV_LOGITS, B.SV_BF16)
+    need = lib.sv_spec_accept_workspace_size(ctypes.byref(d))
+    st = lib.sv_spec_accept(ctypes.byref(d), ctypes.c_void_p(4096 + 8), ok16, ok16, ok16, ok16, ok16, ok16, ok16,
+                            None, ok16, need, None)
+    assert st == B.SV_ERR_INVALID_ARG and "aligned" in B.last_error()

@@ -185,3 +185,24 @@ def test_repeatable_bitwise(dev):
     b = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=256)
     np.testing.assert_array_equal(a[2], b[2])
     np.testing.assert_array_equal(a[3], b[3])
+
+
+def test_request_index_above_32767(dev, orc):
+    """The work list encodes (request, split) in 32 bits: requests at index >= 32768
+    (split partials and merge included) must come out like the others."""
+    from paper_2607_25852_amd import synth
+    R, tail = 32800, 40
+    L = np.full(R, 5, np.int32)
+    L[R - tail:] = np.random.default_rng(7).integers(100, 300, size=tail)
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name="many_reqs", R=R, b=2, dtype="bf16",
+                              Hq=4, Hkv=1, d=64, page=16, kv=("list",) + tuple(int(x) for x in L))
+    say("attn gen many_reqs")
+    kv = synth.make_kv(cfg, L)
+    qo = synth.indptr_from_depths(np.where(np.arange(R) % 2 == 0, 2, 1).astype(np.int32))
+    say("attn run many_reqs")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=64)
+    sel = list(range(R - tail, R)) + [0, 1, 12345, 32767]
+    rows = np.concatenate([np.arange(qo[i], qo[i + 1]) for i in sel]).astype(np.int32)
+    rows = np.repeat(rows, cfg.Hq).astype(np.int32)
+    heads = np.tile(np.arange(cfg.Hq), len(rows) // cfg.Hq).astype(np.int32)
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=(rows, heads))
