@@ -14,6 +14,8 @@
 // second kernel (log-sum-exp weights).
 //
 // fp32 path (vector ALU): one wavefront per (query row, head), 64 keys per step.
+#include <atomic>
+
 #include "sv_internal.h"
 
 namespace sv {
@@ -42,7 +44,7 @@ struct AttnArgs {
     float* part_lse;  // [max_splits, total_q_max, Hq]  (log2 domain)
     int R, total_q, Hq, Hkv, G, block;
     int log2P, maxp, num_pages, max_kv_len;
-    int split, max_splits, nrb;  // nrb: 128-row blocks per (request, kv-head)
+    int split, max_splits, nrb;  // nrb: row blocks (16 rows per wave) per (request, kv-head)
     float scale_log2;  // sm_scale * log2(e)
     float scale;       // sm_scale
 };
@@ -97,15 +99,19 @@ __device__ inline void wait_vm() {
 }
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef short i16x8 __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-// One work item (request i, kv-head h, split s, 128-row block rb). NBUF-deep LDS ring:
-// tile t is multiplied while tiles t+1 .. t+NBUF-1 stream in. Wave w owns query rows
-// 32*(w/2) .. +31 of the row block and token half w%2 of every tile (so a 64-row group
-// keeps all four SIMDs busy, two waves each); the two halves of a row group merge their
-// softmax states at the end. Every early return is uniform over the workgroup.
-template <int HD, int NW, int NBUF, bool ONEPAGE>
-__device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& lds, int i, int h, int s, int rb) {
+// One work item (request i, kv-head h, split s, up to (NW/HALVES)*32 query rows from row0
+// of the kv-head group). NBUF-deep LDS ring:
+// tile t is multiplied while tiles t+1 .. t+NBUF-1 stream in. HALVES == 2: wave w owns
+// query rows 32*(w/2) .. +31 of the row block and token half w%2 of every tile (so a
+// 64-row group keeps all four SIMDs busy, two waves each); the two halves of a row group
+// merge their softmax states at the end. HALVES == 1: wave w owns rows 32*w .. +31 over
+// the whole tile (256 rows per workgroup). Every early return is uniform over the
+// workgroup.
+template <int HD, int NW, int NBUF, bool ONEPAGE, int HALVES>
+__device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& lds, int i, int h, int s, int row0) {
     constexpr int CPR = HD / 8;             // 16-byte chunks per token row
     constexpr int TPS = 1024 / (HD * 2);    // tokens per 1 KB DMA segment
     constexpr int NSEG = kTile / TPS;       // segments per tensor per tile
@@ -126,7 +132,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     if (tok_begin >= kv_len) return;
     const int tok_end = min(kv_len, tok_begin + a.split);
     const int nsplit = (kv_len + a.split - 1) / a.split;
-    const int M = a.G * k_i - rb * 128;  // rows of this row block
+    constexpr int RB = (NW / HALVES) * 32;    // query rows this mapping covers
+    const int M = min(a.G * k_i - row0, RB);  // rows of this item
     if (M <= 0) return;
 
     // page ids of this split -> LDS (the host keeps a split within 1024 pages)
@@ -140,14 +147,16 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     }
 
     // this lane's query row (N index of the MFMA) and its half (K-slice selector)
-    const int rg = w >> 1, th = w & 1;  // row group, token half of each tile
+    // row group; token half of each tile (HALVES == 2), else the whole tile
+    const int rg = w / HALVES, th = HALVES == 2 ? (w & 1) : 0;
     const int r = rg * 32 + (lane & 31);
     const int half = lane >> 5;
     const bool row_ok = r < M;
-    const int rr = rb * 128 + (row_ok ? r : 0);  // row within the request's kv-head group
+    const int rr = row0 + (row_ok ? r : 0);  // row within the request's kv-head group
     const int jq = rr / a.G;
     const int head = h * a.G + rr % a.G;
     const int limit = L + jq;  // last visible key of this row (inclusive)
+    const int last_key = min(limit, tok_end - 1);  // ... and of this split
 
     const uint16_t* __restrict__ qp = (const uint16_t*)a.q;
     const uint16_t* __restrict__ kcp = (const uint16_t*)a.kc;
@@ -221,93 +230,113 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
         }
     };
 
+    constexpr int NSB = 2 / HALVES;  // 32-token halves of a tile handled by this wave
     auto compute_tile = [&](int buf, int tb) {
         if (rg * 32 >= M) return;
         const uint16_t* kt = lds.kv[buf][0];
         const uint16_t* vt = lds.kv[buf][1];
-        // S^T = K Q^T for this wave's 32-token half of the tile (unscaled)
-        f32x16 sacc = f32x16{};
+        // S^T = K Q^T for each 32-token half this wave owns (unscaled). Two independent
+        // accumulation chains keep the matrix pipe busy while K fragments arrive: the two
+        // halves (whole-tile waves), or the even and odd k-steps of one half.
+        f32x16 sacc[NSB];
         {
-            const int t = th * 32 + (lane & 31);
-            const uint16_t* krow = kt + t * HD;
-            const int sw = swz(t) & (CPR - 1);
+            const int sw = swz(lane & 31) & (CPR - 1);  // swz depends on t % 16 only
+            const uint16_t* krow0 = kt + ((HALVES == 2 ? th : 0) * 32 + (lane & 31)) * HD;
+            if constexpr (NSB == 2) {
+                sacc[0] = f32x16{};
+                sacc[1] = f32x16{};
 #pragma unroll
-            for (int kk = 0; kk < KK; kk++) {
-                const bf16x8 af = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow + (((2 * kk + half) ^ sw) << 3)));
-                sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[kk], sacc, 0, 0, 0);
+                for (int kk = 0; kk < KK; kk++) {
+                    const int off = ((2 * kk + half) ^ sw) << 3;
+                    const bf16x8 a0 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + off));
+                    const bf16x8 a1 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + 32 * HD + off));
+                    sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kk], sacc[0], 0, 0, 0);
+                    sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kk], sacc[1], 0, 0, 0);
+                }
+            } else {
+                f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+                for (int kk = 0; kk < KK; kk += 2) {
+                    const bf16x8 a0 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + (((2 * kk + half) ^ sw) << 3)));
+                    const bf16x8 a1 =
+                        __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + (((2 * kk + 2 + half) ^ sw) << 3)));
+                    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kk], s0, 0, 0, 0);
+                    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kk + 1], s1, 0, 0, 0);
+                }
+                sacc[0] = s0 + s1;
             }
         }
-        // causal/tail mask on the raw scores (register e holds token 32th + 8(e/4) + 4*half + e%4)
-        const int tb_h = tb + th * 32;
-        const bool need_mask = (tb_h + 31 > L) || (tb_h + 32 > tok_end) || !row_ok;
-        if (need_mask) {
-#pragma unroll
-            for (int e = 0; e < 16; e++) {
-                const int tok = tb_h + 8 * (e >> 2) + 4 * half + (e & 3);
-                if (!row_ok || tok > limit || tok >= tok_end) sacc[e] = -INFINITY;
-            }
-        }
-        float mx = fmaxf(fmaxf(sacc[0], sacc[1]), sacc[2]);
-#pragma unroll
-        for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[e]), sacc[e + 1]);
-        mx = fmaxf(mx, sacc[15]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float mxs = mx * a.scale_log2;  // tile max in scaled log2 units (-inf: all masked)
-        // lazy rescale: the running max moves only when a score exceeds it by more than 8,
-        // so p = 2^(z - m) <= 256 stays exact in fp32 and bf16, and most tiles skip the
-        // rescale of the accumulators
-        if (__any(mxs > m_run + 8.0f)) {
-            const float m_new = fmaxf(m_run, mxs);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            l_run *= alpha;
-#pragma unroll
-            for (int t = 0; t < DT; t++) o[t] *= alpha;
-            m_run = m_new;
-        }
-        const float nm = -m_run;
-        float psum = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 16; e++) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[e], a.scale_log2, nm));
-            sacc[e] = p;
-            psum += p;
-        }
-        l_run += psum;
-        const bool tail = tb_h + 32 > tok_end;  // V rows past the split end hold foreign data
-
-        // O^T += V^T P^T over this half's two 16-token k-chunks. The V^T operand comes
-        // from two transpose reads: in 16-lane group g = lane/16, input lane j addresses
-        // token 16c + 8q + 4(g/2) + j/4 at dims 32t + 16(g%2) + 4(j%4) .. +3, and output
-        // lane j receives dim 32t + 16(g%2) + j of tokens 16c + 8q + 4(g/2) + 0..3.
+        // Each owned half is one online-softmax step (its own max, lazy rescale, exponent
+        // and PV update), so the softmax of the first half overlaps the MFMAs of the second.
+        // Causal/tail mask on the raw scores: register e of half hh holds token
+        // tb + 32hh + 4*half + (8(e/4) + e%4), masked when that token is past the row's last
+        // visible key or the split end. Only halves reaching past L (the first row's limit)
+        // or the split end need it, a wave-uniform test. Padding rows (r >= M) are not
+        // masked: their query is zero, and their output column is neither written nor
+        // mixed into the other columns.
         const int g = lane >> 4, jl = lane & 15;
 #pragma unroll
-        for (int cc = 0; cc < 2; cc++) {
-            const int c = 2 * th + cc;
-            bf16x8 pb;
+        for (int sb = 0; sb < NSB; sb++) {
+            const int hh = HALVES == 2 ? th : sb;
+            const int tb_h = tb + hh * 32;
+            if (tb_h + 31 > L || tb_h + 32 > tok_end) {
+                const int dlim = last_key - tb_h - 4 * half;  // mask where 8(e/4) + e%4 > dlim
 #pragma unroll
-            for (int e = 0; e < 8; e++) pb[e] = (__bf16)sacc[8 * cc + e];
+                for (int e = 0; e < 16; e++)
+                    if (8 * (e >> 2) + (e & 3) > dlim) sacc[sb][e] = -INFINITY;
+            }
+            float mx = fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), sacc[sb][2]);
 #pragma unroll
-            for (int t = 0; t < DT; t++) {
-                i16x4 vq[2];
+            for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[sb][e]), sacc[sb][e + 1]);
+            mx = fmaxf(mx, sacc[sb][15]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const float mxs = mx * a.scale_log2;  // max in scaled log2 units (-inf: all masked)
+            // lazy rescale: the running max moves only when a score exceeds it by more than
+            // 8, so p = 2^(z - m) <= 256 stays exact in fp32 and bf16, and most steps skip
+            // the rescale of the accumulators
+            if (__any(mxs > m_run + 8.0f)) {
+                const float m_new = fmaxf(m_run, mxs);
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
 #pragma unroll
-                for (int qh = 0; qh < 2; qh++) {
-                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
-                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
-                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
-                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
-                    vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
+                for (int t = 0; t < DT; t++) o[t] *= alpha;
+                m_run = m_new;
+            }
+            const float nm = -m_run;
+            float psum = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[sb][e], a.scale_log2, nm));
+                sacc[sb][e] = p;
+                psum += p;
+            }
+            l_run += psum;
+
+            // O^T += V^T P^T over the two 16-token k-chunks of this half. The V^T operand
+            // comes from two transpose reads: in 16-lane group g = lane/16, input lane j
+            // addresses token 16c + 8q + 4(g/2) + j/4 at dims 32t + 16(g%2) + 4(j%4) .. +3,
+            // and output lane j receives dim 32t + 16(g%2) + j of tokens
+            // 16c + 8q + 4(g/2) + 0..3.
+#pragma unroll
+            for (int cc = 0; cc < 2; cc++) {
+                const int c = 2 * hh + cc;
+                bf16x8 pb;
+#pragma unroll
+                for (int e = 0; e < 8; e++) pb[e] = (__bf16)sacc[sb][8 * cc + e];
+#pragma unroll
+                for (int t = 0; t < DT; t++) {
+                    i16x4 vq[2];
+#pragma unroll
+                    for (int qh = 0; qh < 2; qh++) {
+                        const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
+                        const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
+                        const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
+                        const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                        vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
+                    }
+                    const i16x8 vv = __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
+                    o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, o[t], 0, 0, 0);
                 }
-                if (tail) {
-#pragma unroll
-                    for (int qh = 0; qh < 2; qh++)
-#pragma unroll
-                        for (int e = 0; e < 4; e++)
-                            if (tb + 16 * c + 8 * qh + 4 * (g >> 1) + e >= tok_end) vq[qh][e] = 0;
-                }
-                const i16x4 lo = vq[0], hi = vq[1];
-                const u16x8 vv = {(uint16_t)lo[0], (uint16_t)lo[1], (uint16_t)lo[2], (uint16_t)lo[3],
-                                  (uint16_t)hi[0], (uint16_t)hi[1], (uint16_t)hi[2], (uint16_t)hi[3]};
-                o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, o[t], 0, 0, 0);
             }
         }
     };
@@ -329,31 +358,43 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
             if (newer >= 1) wait_vm<IPW>();
             else wait_vm<0>();
         }
+        // the last tile may reach past the split end: the lanes that copied those V rows
+        // (foreign data, possibly non-finite) zero them, so P = 0 there contributes exactly 0
+        if (t == ntiles - 1 && tok_begin + (t + 1) * kTile > tok_end && my_tensor == 1) {
+            const int tb = tok_begin + t * kTile;
+            char* vbuf = (char*)&lds.kv[0][0][0] + (t % NBUF) * 2 * LdsRing<HD, NBUF>::kTileBytes;
+#pragma unroll
+            for (int k = 0; k < IPW; k++)
+                if (tb + tk[k] >= tok_end) *(u16x8*)(vbuf + ldsoff[k] + 16 * lane) = u16x8{};
+        }
         __syncthreads();
         if (t + PF < ntiles) issue_tile(t + PF, (t + PF) % NBUF);
         compute_tile(t % NBUF, tok_begin + t * kTile);
     }
 
-    // merge the token halves of each row group: the odd wave parks (m, l, O) in LDS (the
-    // ring is free now), the even wave combines and writes. Both waves hold the same
-    // (row, dim) elements in the same lanes and registers.
+    // HALVES == 2: merge the token halves of each row group. The odd wave parks O in the
+    // ring and (m, l) in the page-id area (both free now), the even wave combines and
+    // writes. Both waves hold the same (row, dim) elements in the same lanes and registers.
     float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-    __syncthreads();
-    float* park = (float*)&lds.kv[0][0][0] + (size_t)rg * (64 * 16 * DT + 96);
     const bool grp_ok = rg * 32 < M;
-    if (grp_ok && th == 1) {
+    if constexpr (HALVES == 2) {
+        static_assert((NW / 2) * 64 * 16 * DT * sizeof(float) <= sizeof(lds.kv), "park O");
+        static_assert((NW / 2) * 96 * sizeof(float) <= sizeof(lds.pid), "park m, l");
+        __syncthreads();
+        float* park = (float*)&lds.kv[0][0][0] + (size_t)rg * (64 * 16 * DT);
+        float* park_ml = (float*)&lds.pid[0] + rg * 96;
+        if (grp_ok && th == 1) {
 #pragma unroll
-        for (int t = 0; t < DT; t++)
+            for (int t = 0; t < DT; t++)
 #pragma unroll
-            for (int e = 0; e < 16; e++) park[(t * 16 + e) * 64 + lane] = o[t][e];
-        park[64 * 16 * DT + lane] = m_run;
-        if (lane < 32) park[64 * 16 * DT + 64 + lane] = l_tot;  // rows in lanes 0..31
-    }
-    __syncthreads();
-    if (!grp_ok || th == 1 || !row_ok) return;
-    {
-        const float m2 = park[64 * 16 * DT + lane];
-        const float l2 = park[64 * 16 * DT + 64 + (lane & 31)];
+                for (int e = 0; e < 16; e++) park[(t * 16 + e) * 64 + lane] = o[t][e];
+            park_ml[lane] = m_run;
+            if (lane < 32) park_ml[64 + lane] = l_tot;  // rows in lanes 0..31
+        }
+        __syncthreads();
+        if (!grp_ok || th == 1 || !row_ok) return;
+        const float m2 = park_ml[lane];
+        const float l2 = park_ml[64 + (lane & 31)];
         const float mm = fmaxf(m_run, m2);
         const float a1 = __builtin_amdgcn_exp2f(m_run - mm), a2 = __builtin_amdgcn_exp2f(m2 - mm);
 #pragma unroll
@@ -362,6 +403,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
             for (int e = 0; e < 16; e++) o[t][e] = o[t][e] * a1 + park[(t * 16 + e) * 64 + lane] * a2;
         l_tot = l_tot * a1 + l2 * a2;
         m_run = mm;
+    } else {
+        if (!grp_ok || !row_ok) return;
     }
     const float inv = l_tot > 0.0f ? 1.0f / l_tot : 0.0f;
     const float lse2 = l_tot > 0.0f ? m_run + __log2f(l_tot) : -INFINITY;
@@ -469,7 +512,9 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnArgs a, int32_t* gr
 
 // Persistent: one workgroup per CU pulls work items from the counter until the list is
 // exhausted (every wave leaves through the same test).
-template <int HD, int NW, int NBUF, bool ONEPAGE>
+// WIDE: row blocks of 256 rows; an item with more than 128 rows left uses whole-tile
+// waves, otherwise half-tile waves (all eight busy on up to 128 rows).
+template <int HD, int NW, int NBUF, bool ONEPAGE, bool WIDE>
 __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ groups,
                                                                int32_t* __restrict__ ctr) {
     __shared__ __attribute__((aligned(16))) LdsRing<HD, NBUF> lds;
@@ -484,7 +529,12 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
         if (item >= nitems) break;
         const uint32_t gv = (uint32_t)groups[item / per_group];  // request << 16 | split
         const int within = item % per_group;
-        attn_item<HD, NW, NBUF, ONEPAGE>(a, lds, (int)(gv >> 16), within / a.nrb, (int)(gv & 0xFFFFu), within % a.nrb);
+        const int i = (int)(gv >> 16), h = within / a.nrb, s = (int)(gv & 0xFFFFu);
+        const int row0 = (within % a.nrb) * (WIDE ? 2 * NW * 16 : NW * 16);
+        if (WIDE && a.G * (a.qo[i + 1] - a.qo[i]) - row0 > NW * 16)
+            attn_item<HD, NW, NBUF, ONEPAGE, 1>(a, lds, i, h, s, row0);
+        else
+            attn_item<HD, NW, NBUF, ONEPAGE, 2>(a, lds, i, h, s, row0);
     }
 }
 
@@ -638,8 +688,14 @@ int ilog2(int x) {
 AttnPlan plan_attn(const sv_attn_desc& d) {
     AttnPlan p{};
     const int maxM = (d.num_q_heads / d.num_kv_heads) * d.block;
-    p.waves = 8;  // (32-row group, token half) per wave: 128 query rows per workgroup
-    p.row_blocks = (maxM + 127) / 128;
+    // 8 waves. Up to 128 query rows per kv-head group: a wave owns (32-row group, 32-token
+    // half of each tile), so 64 rows already keep all four SIMDs busy. Above 128 rows a
+    // wave owns 32 rows over the whole tile (256 rows per workgroup), so a group of up to
+    // 256 rows streams its KV once.
+    p.waves = 8;
+    p.halves = maxM > 128 ? 1 : 2;
+    const int rows = (p.waves / p.halves) * 32;
+    p.row_blocks = (maxM + rows - 1) / rows;
     if (d.dtype == SV_F32) {
         p.kv_split = 0;
         p.max_splits = 1;
@@ -712,31 +768,43 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
     }
     a.nrb = plan.row_blocks;
     // persistent grid: one workgroup per compute unit of the current device
-    static int cu_count[64] = {0};
+    static std::atomic<int> cu_count[64];  // zero-initialised (static storage)
     int dev = 0;
     hipError_t e0 = hipGetDevice(&dev);
     if (e0 != hipSuccess) return e0;
     if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (cu_count[dev] == 0) {
+    int ncu = cu_count[dev].load(std::memory_order_relaxed);
+    if (ncu == 0) {
         int n = 0;
         e0 = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
         if (e0 != hipSuccess) return e0;
-        cu_count[dev] = n > 0 ? n : 1;
+        ncu = n > 0 ? n : 1;
+        cu_count[dev].store(ncu, std::memory_order_relaxed);
     }
     char* wsb = (char*)ws;
     int32_t* groups = (int32_t*)(wsb + plan.off_groups);
     int32_t* ctr = (int32_t*)(wsb + plan.off_ctr);
     hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, stream, a, groups, ctr);
-    const dim3 grid(cu_count[dev]);
-#define SV_LAUNCH_ATTN(HDV, NWV, ONEP) \
-    hipLaunchKernelGGL((attn_bf16_kernel<HDV, NWV, 4, ONEP>), grid, dim3(NWV * 64), 0, stream, a, groups, ctr)
+    const dim3 grid(ncu);
+#define SV_LAUNCH_ATTN(HDV, ONEP, HALV) \
+    hipLaunchKernelGGL((attn_bf16_kernel<HDV, 8, 4, ONEP, HALV == 1>), grid, dim3(8 * 64), 0, stream, a, groups, ctr)
     const bool onepage = d.page_size >= kTile;
-    if (d.head_dim == 128) {
-        if (onepage) SV_LAUNCH_ATTN(128, 8, true);
-        else SV_LAUNCH_ATTN(128, 8, false);
+    if (plan.halves == 2) {
+        if (d.head_dim == 128) {
+            if (onepage) SV_LAUNCH_ATTN(128, true, 2);
+            else SV_LAUNCH_ATTN(128, false, 2);
+        } else {
+            if (onepage) SV_LAUNCH_ATTN(64, true, 2);
+            else SV_LAUNCH_ATTN(64, false, 2);
+        }
     } else {
-        if (onepage) SV_LAUNCH_ATTN(64, 8, true);
-        else SV_LAUNCH_ATTN(64, 8, false);
+        if (d.head_dim == 128) {
+            if (onepage) SV_LAUNCH_ATTN(128, true, 1);
+            else SV_LAUNCH_ATTN(128, false, 1);
+        } else {
+            if (onepage) SV_LAUNCH_ATTN(64, true, 1);
+            else SV_LAUNCH_ATTN(64, false, 1);
+        }
     }
 #undef SV_LAUNCH_ATTN
     hipError_t e = hipGetLastError();

@@ -20,7 +20,8 @@ struct AttnPlan {
     int kv_split;     // tokens per split-KV work item (multiple of 64)
     int max_splits;   // ceil(max_kv_len / kv_split)
     int waves;        // waves per workgroup (bf16 path)
-    int row_blocks;   // 128-query-row blocks per (request, kv-head)
+    int halves;       // 2: a wave owns a 32-token half of each tile, 1: the whole tile
+    int row_blocks;   // query-row blocks of (waves / halves) * 32 rows per (request, kv-head)
     size_t part_o_bytes;    // split partial outputs (fp32), offset 0
     size_t part_lse_bytes;  // split partial log-sum-exps, after part_o
     size_t off_groups;      // work list of the persistent kernel

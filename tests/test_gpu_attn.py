@@ -206,3 +206,21 @@ def test_request_index_above_32767(dev, orc):
     rows = np.repeat(rows, cfg.Hq).astype(np.int32)
     heads = np.tile(np.arange(cfg.Hq), len(rows) // cfg.Hq).astype(np.int32)
     check(orc, cfg, kv, qo, kvl, q, o, l, units=(rows, heads))
+
+
+@pytest.mark.parametrize("page,d", [(64, 128), (16, 128), (64, 64), (16, 64)])
+def test_wide_group_whole_tile_waves(dev, orc, page, d):
+    """More than 128 query rows per kv-head group (G = 32, block 16: up to 512 rows):
+    waves own whole tiles, 256 rows per row block, partly filled blocks included."""
+    from paper_2607_25852_amd import synth
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name=f"wide_p{page}_d{d}", b=16, dtype="bf16", Hq=32, Hkv=1,
+                              d=d, page=page)
+    L = synth.kv_context_lengths(cfg)
+    kv = synth.make_kv(cfg, L, fill_unused=np.nan)
+    qo = synth.indptr_from_depths(np.array([16, 3, 9, 12]))
+    say("attn wide", page, d)
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l)
+    # the same rows through several splits agree with the single-split result
+    q2, kvl2, o2, l2 = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=128)
+    assert np.abs(o2 - o).max() <= 2e-2 and np.abs(l2 - l).max() <= 1e-3
