@@ -703,12 +703,12 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     }
     int split = d.kv_split;
     if (split <= 0) {
-        // at most ~8 splits for the longest request, 4096..16384 tokens each: the
-        // persistent kernel balances the work items dynamically, and fewer splits keep
-        // the partial results (written, then merged) small
-        long long want = ((long long)d.max_kv_len + 7) / 8;
+        // about 16 splits for the longest request, 4096..8192 tokens each: enough work
+        // items for the persistent grid to balance (largest first), while the partial
+        // results (written, then merged) stay a few percent of the KV bytes
+        long long want = ((long long)d.max_kv_len + 15) / 16;
         if (want < 4096) want = 4096;
-        if (want > 16384) want = 16384;
+        if (want > 8192) want = 8192;
         split = (int)(((want + 63) / 64) * 64);
     }
     if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
