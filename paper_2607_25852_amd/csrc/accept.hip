@@ -92,7 +92,7 @@ __device__ inline const T* row_ptr(const void* base, long long row, int V) {
 }
 
 // ----------------------------------------------------------------------------------
-// rowstats: grid (NC, R*b + R*D)
+// rowstats: flat grid of (row slot, chunk), R*b + R*D slots of NC chunks
 // ----------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
     typedef T vec_t __attribute__((ext_vector_type(VEC)));
     __shared__ float red[kThreads / 64];
 
-    const int slot = blockIdx.y;
+    const int slot = blockIdx.x / a.NC, c = blockIdx.x % a.NC;  // flat grid: (row slot, chunk)
     const int RB = a.R * a.b;
     const T* row;
     float2* dst;
@@ -117,7 +117,6 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
         row = row_ptr<T>(a.draft, (long long)i * a.D + t, a.V);
         dst = a.stats_q + (size_t)(i * a.D + t) * a.NC;
     }
-    const int c = blockIdx.x;
     const int beg = c * a.stats_chunk;
     const int end = min(a.V, beg + a.stats_chunk);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -368,13 +367,13 @@ __device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
 }
 
 // ----------------------------------------------------------------------------------
-// chunk sums: grid (NCR, R); each workgroup sums the integer residual (or bonus) weights
-// of one vocabulary chunk of one request
+// chunk sums: flat grid of (request, chunk); each workgroup sums the integer residual (or
+// bonus) weights of one vocabulary chunk of one request
 // ----------------------------------------------------------------------------------
 template <bool LOGITS, typename T>
 __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     __shared__ uint64_t red[kThreads / 64];
-    const int i = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+    const int i = blockIdx.x / a.NCR, c = blockIdx.x % a.NCR, tid = threadIdx.x;  // flat grid: (request, chunk)
     const ReqPlan pl = a.plan[i];
     if (pl.mode == 2) return;
     const int beg = c * kResChunk, end = min(a.V, beg + kResChunk);
@@ -580,7 +579,8 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     const bool logits = d.kind == SV_LOGITS;
     const bool bf = d.dtype == SV_BF16;
     if (logits) {
-        const dim3 g(p.stats_chunks, d.num_reqs * d.block + d.num_reqs * (d.block > 1 ? d.block - 1 : 0));
+        const long long slots = (long long)d.num_reqs * d.block + (long long)d.num_reqs * (d.block > 1 ? d.block - 1 : 0);
+        const dim3 g((unsigned)(slots * p.stats_chunks));
         if (bf) hipLaunchKernelGGL(rowstats_kernel<uint16_t>, g, dim3(kThreads), 0, stream, a);
         else hipLaunchKernelGGL(rowstats_kernel<float>, g, dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
@@ -588,8 +588,8 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     }
 #define SV_ACCEPT_PHASES(LG, TT)                                                                      \
     hipLaunchKernelGGL((decide_kernel<LG, TT>), dim3(d.num_reqs), dim3(64), 0, stream, a);            \
-    hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3(p.res_chunks, d.num_reqs), dim3(kThreads), 0, \
-                       stream, a);                                                                    \
+    hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
+                       dim3(kThreads), 0, stream, a);                                                 \
     hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
     if (logits && bf) {
         SV_ACCEPT_PHASES(true, uint16_t);

@@ -133,6 +133,12 @@ sv_status check_accept(const sv_accept_desc* d) {
     }
     if ((long long)d->num_reqs * d->block > (1LL << 30))
         return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: too many rows");
+    // each kernel is one flat grid: its work-item count must fit the 32-bit dispatch size
+    const sv::AcceptPlan p = sv::plan_accept(*d);
+    const long long slots = (long long)d->num_reqs * (2LL * d->block - 1);
+    if (slots * p.stats_chunks * 256 > 0xFFFFFFFFLL || (long long)d->num_reqs * p.res_chunks * 256 > 0xFFFFFFFFLL)
+        return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: %d requests x vocab %d exceed one launch", d->num_reqs,
+                    d->vocab);
     return SV_OK;
 }
 

@@ -210,3 +210,45 @@ def test_repeatable_bitwise(dev):
     cfg, target, draft, toks, qo, ua, us, dtype = _workload(cfg_name, "logits")
     a, b = gpu_accept(dev, target, draft, toks, qo, ua, us, "logits", dtype, repeat=2)
     assert_exact(a, b)
+
+
+def test_many_requests_flat_grids(dev, orc):
+    """70000 requests of block 2 (more row slots than one grid dimension holds):
+    the flat grids of both kernels still cover every request, bit-exact in probs mode."""
+    rng = np.random.default_rng(11)
+    R, b, V = 70000, 2, 64
+    target_full = _rand_rows(rng, R * b, V).reshape(R, b, V)
+    draft = _rand_rows(rng, R * (b - 1), V).reshape(R, b - 1, V)
+    k = rng.integers(1, b + 1, size=R)
+    from paper_2607_25852_amd import synth
+    qo = synth.indptr_from_depths(k.astype(np.int32))
+    target = np.concatenate([target_full[i, :k[i]] for i in range(R)])
+    tokens = rng.integers(0, V, size=(R, b - 1)).astype(np.int32)
+    ua = (rng.integers(0, 1 << 24, size=(R, b - 1)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept many requests", R)
+    g = gpu_accept(dev, target, draft, tokens, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, draft, tokens, qo, ua, us, kind="probs", dtype="f32")
+    assert_exact(g, o)
+
+
+def test_many_requests_flat_grids_logits(dev, orc):
+    """Logits mode at 40000 requests of block 3: the statistics pass covers 200000 row
+    slots on one flat grid."""
+    rng = np.random.default_rng(12)
+    R, b, V = 40000, 3, 96
+    D = b - 1
+    k = rng.integers(1, b + 1, size=R)
+    from paper_2607_25852_amd import synth
+    qo = synth.indptr_from_depths(k.astype(np.int32))
+    tl = (rng.standard_normal((int(qo[-1]), V)) * 2).astype(np.float32)
+    dl = (rng.standard_normal((R, D, V)) * 2).astype(np.float32)
+    toks = rng.integers(0, V, size=(R, D)).astype(np.int32)
+    ua = (rng.integers(0, 1 << 24, size=(R, D)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept many requests logits", R)
+    g = gpu_accept(dev, tl, dl, toks, qo, ua, us, "logits", "f32")
+    o = orc.accept(tl, dl, toks, qo, ua, us, kind="logits", dtype="f32", diagnostics=True)
+    exact, marginal, failures = classify_accept(g, o, ua)
+    assert not failures, failures[:5]
+    assert marginal <= 3
