@@ -283,6 +283,28 @@ def main():
     log(f"step {ms_step:.3f} ms: budget {t_budget * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us "
         f"({a_gbs:.0f} GB/s), acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
 
+    # greedy verification (temperature 0) on the same round, outside the timed steps: the
+    # argmax pass reads only the kept target rows
+    gdesc = binding.accept_desc(cfg.R, cfg.b, cfg.V, binding.SV_LOGITS,
+                                binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16, 0.0)
+    gws = torch.empty(max(binding.accept_workspace_size(gdesc), 256), dtype=torch.uint8, device="cuda")
+
+    def greedy():
+        binding.spec_accept(gdesc, rnd.target, None, rnd.tokens, rnd.qo, None, None, rnd.accept_len,
+                            rnd.out_tokens, rnd.flags, gws)
+
+    for _ in range(3):
+        greedy()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(args.steps):
+        greedy()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    t_greedy = g0.elapsed_time(g1) / args.steps
+    g_bytes = float(rnd.K) * cfg.V * (4 if cfg.dtype == "f32" else 2)
+
     if args.copy_probe:
         log("copy probe")
         copy_probe()
@@ -318,7 +340,10 @@ def main():
                      "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest()},
         "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
-                    "acceptance_algorithmic_bytes": x_bytes},
+                    "acceptance_algorithmic_bytes": x_bytes,
+                    "greedy_acceptance_us": t_greedy * 1e3,
+                    "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
+                    "greedy_acceptance_algorithmic_bytes": g_bytes},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
         "cpu_baseline": cpu,
     }

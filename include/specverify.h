@@ -171,7 +171,8 @@ typedef struct {
     int32_t vocab;      /* V in [1, 2^22]                                      */
     int32_t kind;       /* sv_input_kind: LOGITS (fp32 or bf16) or PROBS (fp32) */
     int32_t dtype;      /* sv_dtype of target and draft                         */
-    float temperature;  /* LOGITS: p = softmax(logits / T), T > 0               */
+    float temperature;  /* T > 0: rejection sampling, LOGITS p = softmax(l / T);
+                           T == 0: greedy verification (either kind)            */
 } sv_accept_desc;
 
 /*
@@ -192,6 +193,12 @@ typedef struct {
  *   A draft token outside [0, V) is rejected (flag bit 2).
  * In LOGITS mode the probabilities are softmax(logits / T) computed in fp32 on
  * the GPU (row max and sum of exponentials per row, read once).
+ * temperature == 0 selects greedy verification (the T -> 0 limit; the paper also
+ * evaluates T = 0): draft t is accepted iff d_t is the argmax of P_{t-1}, and the
+ * extra token is the argmax of P_{a_i}. Argmax = the largest stored value (logit or
+ * probability), lowest index on ties, NaN entries skipped; a row with no non-NaN
+ * entry gives token -1 (flag bit 1). Only the kept target rows are read; draft,
+ * u_accept and u_sample may be NULL.
  *
  * target      [qo_indptr[R], V] rows packed by qo_indptr (fp32 or bf16)
  * draft       [R, b-1, V] (fp32 or bf16); only rows t-1 < n_i are read

@@ -40,6 +40,8 @@ def _load():
     lib.oracle_accept.argtypes = [i32, i32, i32, i32, i32, ctypes.c_float, P, P, P, P, P, P,
                                   P, P, P, P, P, P]
     lib.oracle_accept.restype = i32
+    lib.oracle_accept_greedy.argtypes = [i32, i32, i32, i32, P, P, P, P, P, P]
+    lib.oracle_accept_greedy.restype = i32
     lib.oracle_attn.argtypes = [i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P,
                                 ctypes.c_double, i32, P, P, P, P]
     lib.oracle_attn.restype = i32
@@ -111,6 +113,8 @@ def accept(target, draft, draft_tokens, qo_indptr, u_accept, u_sample, kind="pro
     knd = 1 if kind == "probs" else 0
     edt = np.float32 if dt == 0 else np.uint16
     target = _c(target, edt)
+    if temperature == 0:
+        return accept_greedy(target, np.asarray(draft).shape, draft_tokens, qo_indptr, dtype)
     draft = _c(draft, edt)
     R, D, V = draft.shape
     b = D + 1
@@ -133,6 +137,27 @@ def accept(target, draft, draft_tokens, qo_indptr, u_accept, u_sample, kind="pro
     if diagnostics:
         res.update(p_at=dp, q_at=dq, cdf=dc)
     return res
+
+
+def accept_greedy(target, draft_shape, draft_tokens, qo_indptr, dtype="f32"):
+    """Greedy verification (temperature 0, see oracle.c): argmax of each target row,
+    lowest index on ties, NaN skipped. draft_shape = (R, b-1, V) (draft rows are not
+    read). Returns dict(accept_len, out_tokens, flags)."""
+    dt = 0 if dtype == "f32" else 1
+    edt = np.float32 if dt == 0 else np.uint16
+    target = _c(target, edt)
+    R, D, V = draft_shape
+    b = D + 1
+    dtok = _c(draft_tokens, np.int32).reshape(R, D)
+    qo = _c(qo_indptr, np.int32)
+    acc = np.empty(R, np.int32)
+    out = np.empty((R, b), np.int32)
+    flags = np.empty(R, np.int32)
+    rc = _load().oracle_accept_greedy(R, b, V, dt, _ptr(target), _ptr(dtok), _ptr(qo), _ptr(acc), _ptr(out),
+                                      _ptr(flags))
+    if rc != 0:
+        raise ValueError("oracle_accept_greedy: invalid arguments")
+    return dict(accept_len=acc, out_tokens=out, flags=flags)
 
 
 def attention(q, k_cache, v_cache, page_table, qo_indptr, kv_lens, scale=None, dtype="f32",

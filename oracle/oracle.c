@@ -377,6 +377,67 @@ int oracle_accept(int R, int b, int V, int kind, int dtype, float temperature, c
     return bad ? ORC_EINVAL : ORC_OK;
 }
 
+/*
+ * Greedy verification (temperature 0): the limit of the rule above when both the target
+ * and the draft distributions are one-hot at their argmax (the paper evaluates T = 0).
+ *   argmax of a row: the largest stored value (logits or probabilities; the softmax is
+ *   monotone, so T plays no part), lowest index on ties, NaN entries skipped; -1 when
+ *   every entry is NaN.
+ *   1. accept draft t (t = 1..n_i) iff d_t == argmax P_{t-1};
+ *   2. a_i = (first rejected t) - 1, or n_i;
+ *   3. extra token = argmax P_{a_i} (the residual of two one-hot rows after a rejection,
+ *      the bonus otherwise); -1 sets flag bit 1;
+ *   4. commit as above.  A draft token outside [0, V) is rejected (flag bit 2).
+ * Only the target rows are read.
+ */
+static int row_argmax(const void* base, int dtype, int64_t row, int V) {
+    int best = -1;
+    float bv = 0.0f;
+    for (int v = 0; v < V; v++) {
+        float x = load_elem(base, dtype, row, V, v);
+        if (x != x) continue; /* NaN */
+        if (best < 0 || x > bv) {
+            best = v;
+            bv = x;
+        }
+    }
+    return best;
+}
+
+int oracle_accept_greedy(int R, int b, int V, int dtype, const void* target, const int* draft_tokens,
+                         const int* qo_indptr, int* accept_len, int* out_tokens, int* flags) {
+    if (R < 1 || b < 1 || V < 1) return ORC_EINVAL;
+    const int D = b - 1;
+    for (int i = 0; i < R; i++) {
+        int n = qo_indptr[i + 1] - qo_indptr[i] - 1;
+        if (n < 0 || n > D) return ORC_EINVAL;
+    }
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < R; i++) {
+        const int n = qo_indptr[i + 1] - qo_indptr[i] - 1;
+        int flag = 0;
+        int a = n;
+        for (int t = 1; t <= n; t++) {
+            int d = draft_tokens[(int64_t)i * D + (t - 1)];
+            int acc = 0;
+            if (d < 0 || d >= V) flag |= 4;
+            else acc = (d == row_argmax(target, dtype, (int64_t)qo_indptr[i] + (t - 1), V));
+            if (!acc) {
+                a = t - 1;
+                break;
+            }
+        }
+        int token = row_argmax(target, dtype, (int64_t)qo_indptr[i] + a, V);
+        if (token < 0) flag |= 2;
+        for (int k = 0; k < b; k++) out_tokens[(int64_t)i * b + k] = -1;
+        for (int t = 1; t <= a; t++) out_tokens[(int64_t)i * b + (t - 1)] = draft_tokens[(int64_t)i * D + (t - 1)];
+        out_tokens[(int64_t)i * b + a] = token;
+        accept_len[i] = a;
+        if (flags) flags[i] = flag;
+    }
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------------ */
 /* Verify attention (every kept position is evaluated by the target,   */
 /* Sec. 4.1; packed batch of Sec. 4.2).  Plain definition, fp64:        */

@@ -523,6 +523,141 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
     }
 }
 
+// ----------------------------------------------------------------------------------
+// Greedy verification (temperature 0): rejection sampling with one-hot target and draft
+// rows. Draft t is accepted iff it is the argmax of P_{t-1}; the extra token is the argmax
+// of P_a. Argmax: largest stored value (lowest index on ties, NaN skipped), so only the
+// kept target rows are read and no arithmetic decides anything.
+// ----------------------------------------------------------------------------------
+struct ArgBest {
+    float v;
+    int idx;  // < 0: no non-NaN entry
+};
+
+// the better of two candidates: a valid one, then the larger value, then the lower index
+__device__ inline ArgBest arg_better(ArgBest x, ArgBest y) {
+    if (y.idx < 0) return x;
+    if (x.idx < 0) return y;
+    if (y.v > x.v || (y.v == x.v && y.idx < x.idx)) return y;
+    return x;
+}
+
+__device__ inline ArgBest wave_arg_best(ArgBest x) {
+    for (int off = 32; off > 0; off >>= 1) {
+        ArgBest y;
+        y.v = __shfl_xor(x.v, off, 64);
+        y.idx = __shfl_xor(x.idx, off, 64);
+        x = arg_better(x, y);
+    }
+    return x;
+}
+
+// flat grid of (target row slot, chunk): (max, argmax) of one chunk of a kept target row,
+// stored as (value, index bits) in the statistics slot
+template <typename T>
+__global__ __launch_bounds__(kThreads) void argmax_kernel(AcceptArgs a) {
+    constexpr int VEC = 16 / sizeof(T);
+    typedef T vec_t __attribute__((ext_vector_type(VEC)));
+    __shared__ float s_v[kThreads / 64];
+    __shared__ int s_i[kThreads / 64];
+    const int slot = blockIdx.x / a.NC, c = blockIdx.x % a.NC;
+    if (slot >= a.qo[a.R]) return;
+    const T* row = row_ptr<T>(a.target, slot, a.V);
+    const int beg = c * a.stats_chunk, end = min(a.V, beg + a.stats_chunk);
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // each thread visits its elements in increasing index order: a strict > keeps the
+    // lowest index among equal values
+    ArgBest best{0.0f, -1};
+    if ((a.V % VEC) == 0 && (end - beg) == a.stats_chunk) {
+        const vec_t* rv = (const vec_t*)(row + beg);
+        vec_t v[kStatsLoads];
+#pragma unroll
+        for (int k = 0; k < kStatsLoads; k++) v[k] = rv[tid + k * kThreads];
+#pragma unroll
+        for (int k = 0; k < kStatsLoads; k++)
+#pragma unroll
+            for (int e = 0; e < VEC; e++) {
+                const float x = to_f(v[k][e]);
+                if (x == x && (best.idx < 0 || x > best.v)) {
+                    best.v = x;
+                    best.idx = beg + (tid + k * kThreads) * VEC + e;
+                }
+            }
+    } else {
+        for (int k = 0; k < kStatsLoads; k++)
+            for (int e = 0; e < VEC; e++) {
+                const int vi = beg + (tid + k * kThreads) * VEC + e;
+                if (vi >= end) continue;
+                const float x = load_x<T>(row, vi);
+                if (x == x && (best.idx < 0 || x > best.v)) {
+                    best.v = x;
+                    best.idx = vi;
+                }
+            }
+    }
+    best = wave_arg_best(best);
+    if (lane == 0) {
+        s_v[w] = best.v;
+        s_i[w] = best.idx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        ArgBest b = ArgBest{s_v[0], s_i[0]};
+        for (int k = 1; k < kThreads / 64; k++) b = arg_better(b, ArgBest{s_v[k], s_i[k]});
+        a.stats_t[(size_t)slot * a.NC + c] = make_float2(b.v, __int_as_float(b.idx));
+    }
+}
+
+// one wavefront per request: lane r merges the chunk results of P_r, lane t tests draft
+// t+1 against the argmax of P_t, a ballot finds the first mismatch
+__global__ __launch_bounds__(64) void decide_greedy_kernel(AcceptArgs a) {
+    const int i = blockIdx.x, lane = threadIdx.x;
+    const int q0 = a.qo[i];
+    const int n = a.qo[i + 1] - q0 - 1;
+    const int K = a.qo[a.R];
+    if (n < 0 || n > a.D || q0 < 0 || q0 + n + 1 > K || K > a.R * a.b) {  // malformed packing
+        if (lane == 0) {
+            a.accept_len[i] = 0;
+            if (a.flags) a.flags[i] = 2;
+        }
+        for (int t = lane; t < a.b; t += 64) a.out_tokens[(size_t)i * a.b + t] = -1;
+        return;
+    }
+    ArgBest rb{0.0f, -1};
+    if (lane <= n) {
+        const float2* st = a.stats_t + (size_t)(q0 + lane) * a.NC;
+        for (int c = 0; c < a.NC; c++) {
+            const float2 v = st[c];
+            rb = arg_better(rb, ArgBest{v.x, __float_as_int(v.y)});
+        }
+    }
+    const int am = rb.idx;  // argmax of P_lane
+    bool reject = false, bad_tok = false;
+    if (lane < n) {
+        const int d = a.tokens[(size_t)i * a.D + lane];
+        if (d < 0 || d >= a.V) {
+            reject = true;
+            bad_tok = true;
+        } else {
+            reject = d != am;
+        }
+    }
+    const uint64_t fails = __ballot(reject);
+    const int acc = fails ? __builtin_ctzll(fails) : n;
+    const int token = __shfl(am, acc, 64);
+    const int flag = (token < 0 ? 2 : 0) | (__shfl((int)bad_tok, acc & 63, 64) ? 4 : 0);
+    for (int t = lane; t < a.b; t += 64) {
+        int v = -1;
+        if (t < acc) v = a.tokens[(size_t)i * a.D + t];
+        else if (t == acc) v = token;
+        a.out_tokens[(size_t)i * a.b + t] = v;
+    }
+    if (lane == 0) {
+        a.accept_len[i] = acc;
+        if (a.flags) a.flags[i] = flag;
+    }
+}
+
 }  // namespace
 
 AcceptPlan plan_accept(const sv_accept_desc& d) {
@@ -575,9 +710,16 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     a.stats_chunk = p.stats_chunk;
     a.NCR = p.res_chunks;
     a.res_chunk = p.res_chunk;
-    a.invT = d.kind == SV_LOGITS ? 1.0f / d.temperature : 1.0f;
+    a.invT = d.kind == SV_LOGITS && d.temperature > 0.0f ? 1.0f / d.temperature : 1.0f;
     const bool logits = d.kind == SV_LOGITS;
     const bool bf = d.dtype == SV_BF16;
+    if (d.temperature == 0.0f) {  // greedy verification
+        const dim3 g((unsigned)((long long)d.num_reqs * d.block * p.stats_chunks));
+        if (bf) hipLaunchKernelGGL(argmax_kernel<uint16_t>, g, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL(argmax_kernel<float>, g, dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL(decide_greedy_kernel, dim3(d.num_reqs), dim3(64), 0, stream, a);
+        return hipGetLastError();
+    }
     if (logits) {
         const long long slots = (long long)d.num_reqs * d.block + (long long)d.num_reqs * (d.block > 1 ? d.block - 1 : 0);
         const dim3 g((unsigned)(slots * p.stats_chunks));

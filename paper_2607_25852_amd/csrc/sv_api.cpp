@@ -125,12 +125,12 @@ sv_status check_accept(const sv_accept_desc* d) {
         return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: unknown dtype %d", d->dtype);
     if (d->kind == SV_PROBS) {
         if (d->dtype != SV_F32) return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: probability rows must be fp32");
-    } else if (d->kind == SV_LOGITS) {
-        if (!(d->temperature > 0.0f) || std::isinf(d->temperature))
-            return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: temperature must be finite and > 0");
-    } else {
+    } else if (d->kind != SV_LOGITS) {
         return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: unknown kind %d", d->kind);
     }
+    if (!(d->temperature >= 0.0f) || std::isinf(d->temperature))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_spec_accept: temperature must be finite and >= 0 (0 selects greedy verification)");
     if ((long long)d->num_reqs * d->block > (1LL << 30))
         return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept: too many rows");
     // each kernel is one flat grid: its work-item count must fit the 32-bit dispatch size
@@ -197,8 +197,9 @@ sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const v
     sv_status st = check_accept(desc);
     if (st != SV_OK) return st;
     const bool has_drafts = desc->block > 1;
-    if (!target || !qo_indptr || !u_sample || !accept_len || !out_tokens ||
-        (has_drafts && (!draft || !draft_tokens || !u_accept)))
+    const bool greedy = desc->temperature == 0.0f;  // reads neither draft rows nor uniforms
+    if (!target || !qo_indptr || !accept_len || !out_tokens || (has_drafts && !draft_tokens) ||
+        (!greedy && (!u_sample || (has_drafts && (!draft || !u_accept)))))
         return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: a required pointer is NULL");
     if (!aligned(target, 16) || !aligned(draft, 16) || !aligned(ws, 16) || !aligned(draft_tokens, 4) ||
         !aligned(qo_indptr, 4) || !aligned(u_accept, 4) || !aligned(u_sample, 4) || !aligned(accept_len, 4) ||

@@ -114,7 +114,8 @@ def _accept(lib, d, ws=None, ws_bytes=0):
     (dict(b=0), 1, "block"),
     (dict(V=(1 << 22) + 1), 1, "vocab"),
     (dict(kind=B.SV_PROBS, dtype=B.SV_BF16), 2, "fp32"),
-    (dict(temperature=0.0), 1, "temperature"),
+    (dict(temperature=-1.0), 1, "temperature"),
+    (dict(temperature=float("inf")), 1, "temperature"),
     (dict(temperature=float("nan")), 1, "temperature"),
     (dict(kind=5), 1, "kind"),
 ])

@@ -252,3 +252,70 @@ def test_many_requests_flat_grids_logits(dev, orc):
     exact, marginal, failures = classify_accept(g, o, ua)
     assert not failures, failures[:5]
     assert marginal <= 3
+
+
+def _greedy_tokens(rng, target_f32, qo, D, share=0.75):
+    """draft tokens: the argmax of the target row with probability `share`, else random"""
+    R = len(qo) - 1
+    V = target_f32.shape[1]
+    tok = rng.integers(0, V, size=(R, D)).astype(np.int32)
+    for i in range(R):
+        for t in range(int(qo[i + 1] - qo[i]) - 1):
+            row = target_f32[qo[i] + t]
+            if rng.random() < share and not np.all(np.isnan(row)):
+                tok[i, t] = int(np.nanargmax(row))
+    return tok
+
+
+def gpu_greedy(torch, target, D, tokens, qo, kind, dtype):
+    """greedy call with NULL draft rows and uniforms (they are not read)"""
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd.round import to_dev
+    R, V = len(qo) - 1, target.shape[1]
+    b = D + 1
+    d = B.accept_desc(R, b, V, B.SV_PROBS if kind == "probs" else B.SV_LOGITS,
+                      B.SV_F32 if dtype == "f32" else B.SV_BF16, 0.0)
+    ws = torch.empty(B.accept_workspace_size(d), dtype=torch.uint8, device="cuda")
+    acc = torch.full((R,), -9, dtype=torch.int32, device="cuda")
+    out = torch.full((R, b), -9, dtype=torch.int32, device="cuda")
+    flags = torch.full((R,), -9, dtype=torch.int32, device="cuda")
+    B.spec_accept(d, to_dev(target), None, to_dev(np.ascontiguousarray(tokens, np.int32)),
+                  to_dev(np.ascontiguousarray(qo, np.int32)), None, None, acc, out, flags, ws)
+    torch.cuda.synchronize()
+    return dict(accept_len=acc.cpu().numpy(), out_tokens=out.cpu().numpy(), flags=flags.cpu().numpy())
+
+
+@pytest.mark.parametrize("name", ["tiny", "c16_b16", "c64_b16", "sweep_mtp_c32"])
+def test_greedy_logits_bit_exact(dev, orc, name):
+    """temperature 0 on the workload's logits: argmax decisions are exact on both sides"""
+    from paper_2607_25852_amd import synth
+    cfg, target, draft, _, qo, _, _, dtype = _workload(name, "logits")
+    tf = synth.bf16_to_f32(target) if dtype == "bf16" else target
+    tokens = _greedy_tokens(np.random.default_rng(5), tf, qo, cfg.D, share=0.9)
+    say("accept greedy", name)
+    g = gpu_greedy(dev, target, cfg.D, tokens, qo, "logits", dtype)
+    o = orc.accept_greedy(target, (cfg.R, cfg.D, cfg.V), tokens, qo, dtype=dtype)
+    assert_exact(g, o)
+    assert np.mean(o["accept_len"]) > 1.0  # long accepted prefixes were exercised
+
+
+@pytest.mark.parametrize("V", [1, 7, 1000, 8192, 16385, 40000])
+def test_greedy_ties_nan_ragged(dev, orc, V):
+    """coarse values (many ties), NaN entries, an all-NaN row, out-of-range tokens,
+    ragged vocabulary sizes; fp32 logits, bf16 logits and fp32 probabilities"""
+    from paper_2607_25852_amd import synth
+    rng = np.random.default_rng(V)
+    R, b = 19, 7
+    D = b - 1
+    k = rng.integers(1, b + 1, size=R)
+    qo = synth.indptr_from_depths(k.astype(np.int32))
+    x = rng.integers(-3, 4, size=(int(qo[-1]), V)).astype(np.float32)
+    x[rng.random(x.shape) < 0.05] = np.nan
+    x[int(qo[3])] = np.nan  # a whole row
+    tokens = _greedy_tokens(rng, x, qo, D)
+    tokens[2, 0] = V + 3
+    tokens[5, 0] = -1
+    for kind, dtype, tgt in [("logits", "f32", x), ("logits", "bf16", synth.bf16_bits(x)), ("probs", "f32", x)]:
+        g = gpu_greedy(dev, tgt, D, tokens, qo, kind, dtype)
+        o = orc.accept_greedy(tgt, (R, D, V), tokens, qo, dtype=dtype)
+        assert_exact(g, o)
