@@ -179,6 +179,21 @@ def accept_bytes(cfg, k):
     return float(np.sum((n + 1) + n)) * cfg.V * e
 
 
+def time_loop(torch, stream, fn, steps):
+    """Mean milliseconds of fn() over `steps` back-to-back calls on `stream`, after three
+    untimed calls."""
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(steps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
+
+
 def cpu_baseline(cfg, rnd, min_seconds):
     """The oracle, as it stands, on the same round: budget over the whole batch, then
     attention (every row and head) and acceptance of every request; repeated until at
@@ -236,7 +251,7 @@ def main():
     import numpy as np
     import torch
     from paper_2607_25852_amd import binding, synth
-    from paper_2607_25852_amd.round import DeviceRound
+    from paper_2607_25852_amd.round import DeviceRound, to_dev
 
     binding.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -293,17 +308,41 @@ def main():
         binding.spec_accept(gdesc, rnd.target, None, rnd.tokens, rnd.qo, None, None, rnd.accept_len,
                             rnd.out_tokens, rnd.flags, gws)
 
-    for _ in range(3):
-        greedy()
-    torch.cuda.synchronize()
-    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    g0.record(stream)
-    for _ in range(args.steps):
-        greedy()
-    g1.record(stream)
-    torch.cuda.synchronize()
-    t_greedy = g0.elapsed_time(g1) / args.steps
+    t_greedy = time_loop(torch, stream, greedy, args.steps)
     g_bytes = float(rnd.K) * cfg.V * (4 if cfg.dtype == "f32" else 2)
+
+    # packing of the verify batch and the KV append of the same round, outside the timed
+    # steps; the append writes the kept positions' own keys and values (gathered from the
+    # cache) back to their slots, so the round's cache is unchanged
+    e_sz = 4 if cfg.dtype == "f32" else 2
+    pt_h = rnd.kv["page_table"]
+    k_new_h = np.empty((rnd.K, cfg.Hkv, cfg.d), rnd.kv["k_cache"].dtype)
+    v_new_h = np.empty_like(k_new_h)
+    for i in range(cfg.R):
+        for j in range(int(k[i])):
+            s_ = int(rnd.L[i]) + j
+            k_new_h[rnd.qo_host[i] + j] = rnd.kv["k_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
+            v_new_h[rnd.qo_host[i] + j] = rnd.kv["v_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
+    k_new, v_new = to_dev(k_new_h), to_dev(v_new_h)
+    ctx = to_dev(np.asarray(rnd.L, np.int32))
+    blk_tok = to_dev(np.random.default_rng(cfg.seed).integers(0, cfg.V, size=(cfg.R, cfg.b)).astype(np.int32))
+    p_tok = torch.empty(cfg.R * cfg.b, dtype=torch.int32, device="cuda")
+    p_pos = torch.empty_like(p_tok)
+    p_kvl = torch.empty(cfg.R, dtype=torch.int32, device="cuda")
+    pdesc = binding.pack_desc(cfg.R, cfg.b, cfg.R * cfg.b)
+    apdesc = binding.append_desc(cfg.R, rnd.K, cfg.b, cfg.Hkv, cfg.d, cfg.page, pt_h.shape[1], rnd.kv["num_pages"],
+                                 binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
+
+    def pack():
+        binding.pack_verify(pdesc, blk_tok, ctx, rnd.qo, p_tok, p_pos, p_kvl)
+
+    def append():
+        binding.append_kv(apdesc, k_new, v_new, rnd.page_table, rnd.qo, ctx, rnd.k_cache, rnd.v_cache)
+
+    t_pack = time_loop(torch, stream, pack, args.steps)
+    t_append = time_loop(torch, stream, append, args.steps)
+    assert np.array_equal(p_kvl.cpu().numpy(), rnd.kv_lens_host)
+    ap_bytes = 4.0 * rnd.K * cfg.Hkv * cfg.d * e_sz
 
     if args.copy_probe:
         log("copy probe")
@@ -343,7 +382,9 @@ def main():
                     "acceptance_algorithmic_bytes": x_bytes,
                     "greedy_acceptance_us": t_greedy * 1e3,
                     "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
-                    "greedy_acceptance_algorithmic_bytes": g_bytes},
+                    "greedy_acceptance_algorithmic_bytes": g_bytes,
+                    "pack_us": t_pack * 1e3, "append_us": t_append * 1e3,
+                    "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
         "cpu_baseline": cpu,
     }

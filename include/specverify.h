@@ -3,12 +3,16 @@
  * speculative-decoding draft-verify round on an AMD Instinct MI355X (gfx950).
  *
  * The round (AngelSpec, Sec. 4 "Real-World Deployment: D-cut", and the
- * rejection-sampling verification of Sec. 1) has three steps, one call each:
+ * rejection-sampling verification of Sec. 1) has three steps, one call each,
+ * and two data-movement calls between the budget and the attention:
  *
  *   sv_alloc_budget  D-cut verification budget: prefix confidence scores, a
  *                    global top-K over every request's draft positions, the
  *                    budget ratio chosen against a profiled cost, and the dense
  *                    packing of the kept positions (qo_indptr).
+ *   sv_pack_verify   the dense verify batch (tokens, positions, key counts) of
+ *                    the kept prefixes, the target model's input;
+ *   sv_append_kv     the kept positions' keys and values into the paged cache;
  *   sv_verify_attn   attention of every kept position over its request's paged
  *                    KV cache: causal inside the block, full over the context,
  *                    grouped-query heads.
@@ -115,6 +119,65 @@ typedef struct {
 sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t* keep,
                           int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
                           void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* The dense verify batch of the kept prefixes (Sec. 4.2, "Packing and        */
+/* correctness") and the cache append of their keys and values                */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_reqs;  /* R >= 1                                               */
+    int32_t block;     /* b in [1, 16]                                          */
+    int32_t total_max; /* rows allocated in tokens / positions (>= qo_indptr[R]) */
+} sv_pack_desc;
+
+/*
+ * sv_pack_verify -- the dense verify batch of the kept block prefixes: for request
+ * i with k_i = qo_indptr[i+1]-qo_indptr[i] kept positions and committed context
+ * L_i = ctx_lens[i], row r = qo_indptr[i] + j (0 <= j < k_i) gets
+ *     tokens[r] = block_tokens[i][j]   (position 0: the certain token, then drafts)
+ *     positions[r] = L_i + j           (absolute position in the sequence)
+ * and kv_lens[i] = L_i + k_i, the key count sv_verify_attn reads once the kept
+ * positions' keys and values are in the cache (sv_append_kv).
+ * A request with k_i outside [1, b], or with rows outside [0, total_max), gets no
+ * rows and kv_lens[i] = L_i.
+ * block_tokens [R, b] int32; ctx_lens [R] int32 >= 0; qo_indptr [R+1] int32
+ * tokens, positions [total_max] int32 out (rows that no request owns are untouched);
+ * kv_lens [R] int32 out. All pointers are device memory owned by the caller; the
+ * call is asynchronous on `stream` and allocates nothing.
+ */
+sv_status sv_pack_verify(const sv_pack_desc* desc, const int32_t* block_tokens, const int32_t* ctx_lens,
+                         const int32_t* qo_indptr, int32_t* tokens, int32_t* positions, int32_t* kv_lens,
+                         void* stream);
+
+typedef struct {
+    int32_t num_reqs;          /* R >= 1                                        */
+    int32_t total_max;         /* rows allocated in k_new / v_new               */
+    int32_t block;             /* max k_i (<= 16)                               */
+    int32_t num_kv_heads;      /* Hkv                                           */
+    int32_t head_dim;          /* d; d * element size a multiple of 16 bytes    */
+    int32_t page_size;         /* P, a power of two in [1, 4096]                */
+    int32_t max_pages_per_req; /* columns of page_table                          */
+    int32_t num_pages;         /* pages in each cache                            */
+    int32_t dtype;             /* sv_dtype of the rows and the caches            */
+} sv_append_desc;
+
+/*
+ * sv_append_kv -- write the keys and values of the packed verify rows into the paged
+ * cache (the step between the target's projection and sv_verify_attn): row
+ * r = qo_indptr[i] + j of k_new / v_new, for every kv-head, goes to position
+ * s = ctx_lens[i] + j of request i, i.e. page page_table[i][s / P], slot s % P.
+ * A row whose page id is outside [0, num_pages) or whose page column is outside
+ * [0, max_pages_per_req) is skipped, and so is every row of a request with k_i
+ * outside [1, block], rows outside [0, total_max) or ctx_lens[i] < 0; nothing else
+ * in the caches is written. Two requests that map a position to the same page slot
+ * race (the caller owns the page table). Device memory owned by the caller;
+ * asynchronous on `stream`; allocates nothing.
+ * k_new, v_new [total_max, Hkv, d]; k_cache, v_cache [num_pages, Hkv, P, d]
+ * page_table [R, max_pages_per_req] int32; qo_indptr [R+1]; ctx_lens [R] int32
+ */
+sv_status sv_append_kv(const sv_append_desc* desc, const void* k_new, const void* v_new,
+                       const int32_t* page_table, const int32_t* qo_indptr, const int32_t* ctx_lens,
+                       void* k_cache, void* v_cache, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* Verify attention (every kept position is evaluated by the target model,    */

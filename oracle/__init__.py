@@ -199,3 +199,59 @@ def attention(q, k_cache, v_cache, page_table, qo_indptr, kv_lens, scale=None, d
     if rc != 0:
         raise ValueError("oracle_attn: invalid arguments")
     return out, lse
+
+
+# ------------------------------------------------------------------------------------
+# packing of the verify batch and the cache append (Sec. 4.2, "Packing and correctness")
+# ------------------------------------------------------------------------------------
+def pack_verify(block_tokens, ctx_lens, qo_indptr, total_max):
+    """Dense verify batch: row qo[i] + j (j < k_i) holds block_tokens[i][j] at absolute
+    position ctx_lens[i] + j; kv_lens[i] = ctx_lens[i] + k_i. A request with k_i outside
+    [1, b] or rows outside [0, total_max) gets no rows and kv_lens[i] = ctx_lens[i].
+    Returns (tokens, positions, kv_lens); unwritten rows hold -1."""
+    bt = np.asarray(block_tokens, np.int32)
+    R, b = bt.shape
+    L = np.asarray(ctx_lens, np.int64)
+    qo = np.asarray(qo_indptr, np.int64)
+    tokens = np.full(total_max, -1, np.int32)
+    positions = np.full(total_max, -1, np.int32)
+    kv_lens = np.zeros(R, np.int32)
+    for i in range(R):
+        k = int(qo[i + 1] - qo[i])
+        ok = 1 <= k <= b and qo[i] >= 0 and qo[i] + k <= total_max
+        kv_lens[i] = L[i] + k if ok else L[i]
+        if not ok:
+            continue
+        for j in range(k):
+            tokens[qo[i] + j] = bt[i, j]
+            positions[qo[i] + j] = L[i] + j
+    return tokens, positions, kv_lens
+
+
+def append_kv(k_new, v_new, page_table, qo_indptr, ctx_lens, k_cache, v_cache, block):
+    """Copies of the caches with row qo[i] + j of k_new / v_new (every kv-head) written at
+    position s = ctx_lens[i] + j: page page_table[i][s // P], slot s % P. Rows of a request
+    with k_i outside [1, block], or whose page column or page id is out of range, are
+    skipped."""
+    kc = np.array(k_cache, copy=True)
+    vc = np.array(v_cache, copy=True)
+    num_pages, Hkv, P, d = kc.shape
+    pt = np.asarray(page_table)
+    R, maxp = pt.shape
+    qo = np.asarray(qo_indptr, np.int64)
+    total = np.asarray(k_new).shape[0]
+    for i in range(R):
+        k = int(qo[i + 1] - qo[i])
+        if not (1 <= k <= block and qo[i] >= 0 and qo[i] + k <= total) or ctx_lens[i] < 0:
+            continue
+        for j in range(k):
+            s = int(ctx_lens[i]) + j
+            col = s // P
+            if col >= maxp:
+                continue
+            pg = int(pt[i, col])
+            if pg < 0 or pg >= num_pages:
+                continue
+            kc[pg, :, s % P, :] = k_new[qo[i] + j]
+            vc[pg, :, s % P, :] = v_new[qo[i] + j]
+    return kc, vc

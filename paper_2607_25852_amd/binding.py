@@ -21,8 +21,9 @@ SV_BUDGET_FIXED, SV_BUDGET_COST = 0, 1
 SV_MAX_RATIOS = 8
 
 # every symbol the header declares (checked by the ABI test)
-EXPORTED = ("sv_alloc_budget", "sv_verify_attn", "sv_verify_attn_workspace_size", "sv_spec_accept",
-            "sv_spec_accept_workspace_size", "sv_status_string", "sv_last_error", "sv_abi_version")
+EXPORTED = ("sv_alloc_budget", "sv_pack_verify", "sv_append_kv", "sv_verify_attn", "sv_verify_attn_workspace_size",
+            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_status_string", "sv_last_error",
+            "sv_abi_version")
 
 
 class BudgetDesc(ctypes.Structure):
@@ -44,6 +45,16 @@ class AttnDesc(ctypes.Structure):
 class AcceptDesc(ctypes.Structure):
     _fields_ = [("num_reqs", ctypes.c_int32), ("block", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("temperature", ctypes.c_float)]
+
+
+class PackDesc(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("block", ctypes.c_int32), ("total_max", ctypes.c_int32)]
+
+
+class AppendDesc(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("total_max", ctypes.c_int32), ("block", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("max_pages_per_req", ctypes.c_int32), ("num_pages", ctypes.c_int32), ("dtype", ctypes.c_int32)]
 
 
 class SpecVerifyError(RuntimeError):
@@ -76,6 +87,10 @@ def load() -> ctypes.CDLL:
     lib.sv_spec_accept.restype = i32
     lib.sv_spec_accept_workspace_size.argtypes = [ctypes.POINTER(AcceptDesc)]
     lib.sv_spec_accept_workspace_size.restype = ctypes.c_size_t
+    lib.sv_pack_verify.argtypes = [ctypes.POINTER(PackDesc), P, P, P, P, P, P, P]
+    lib.sv_pack_verify.restype = i32
+    lib.sv_append_kv.argtypes = [ctypes.POINTER(AppendDesc), P, P, P, P, P, P, P, P]
+    lib.sv_append_kv.restype = i32
     lib.sv_status_string.argtypes = [i32]
     lib.sv_status_string.restype = ctypes.c_char_p
     lib.sv_last_error.argtypes = []
@@ -175,6 +190,35 @@ def verify_attn(desc: AttnDesc, q, k_cache, v_cache, page_table, qo_indptr, kv_l
     st = load().sv_verify_attn(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
                                _ptr(qo_indptr), _ptr(kv_lens), _ptr(out), _ptr(lse), _ptr(ws), nbytes,
                                _stream(stream))
+    _check(st)
+
+
+# ------------------------------------------------------------------------------------
+# sv_pack_verify / sv_append_kv
+# ------------------------------------------------------------------------------------
+def pack_desc(R: int, b: int, total_max: int) -> PackDesc:
+    d = PackDesc()
+    d.num_reqs, d.block, d.total_max = R, b, total_max
+    return d
+
+
+def pack_verify(desc: PackDesc, block_tokens, ctx_lens, qo_indptr, tokens, positions, kv_lens, stream=None):
+    st = load().sv_pack_verify(ctypes.byref(desc), _ptr(block_tokens), _ptr(ctx_lens), _ptr(qo_indptr),
+                               _ptr(tokens), _ptr(positions), _ptr(kv_lens), _stream(stream))
+    _check(st)
+
+
+def append_desc(R: int, total_max: int, block: int, Hkv: int, d: int, page_size: int, max_pages_per_req: int,
+                num_pages: int, dtype: int) -> AppendDesc:
+    a = AppendDesc()
+    a.num_reqs, a.total_max, a.block, a.num_kv_heads, a.head_dim = R, total_max, block, Hkv, d
+    a.page_size, a.max_pages_per_req, a.num_pages, a.dtype = page_size, max_pages_per_req, num_pages, dtype
+    return a
+
+
+def append_kv(desc: AppendDesc, k_new, v_new, page_table, qo_indptr, ctx_lens, k_cache, v_cache, stream=None):
+    st = load().sv_append_kv(ctypes.byref(desc), _ptr(k_new), _ptr(v_new), _ptr(page_table), _ptr(qo_indptr),
+                             _ptr(ctx_lens), _ptr(k_cache), _ptr(v_cache), _stream(stream))
     _check(st)
 
 

@@ -184,6 +184,62 @@ sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_
                     "sv_verify_attn");
 }
 
+sv_status sv_pack_verify(const sv_pack_desc* desc, const int32_t* block_tokens, const int32_t* ctx_lens,
+                         const int32_t* qo_indptr, int32_t* tokens, int32_t* positions, int32_t* kv_lens,
+                         void* stream) {
+    if (!desc) return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: desc is NULL");
+    const sv_pack_desc& d = *desc;
+    if (d.num_reqs < 1) return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: num_reqs %d < 1", d.num_reqs);
+    if (d.block < 1 || d.block > SV_MAX_BLOCK)
+        return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: block %d outside [1, %d]", d.block, SV_MAX_BLOCK);
+    if (d.total_max < 1) return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: total_max %d < 1", d.total_max);
+    if ((long long)d.num_reqs * d.block > (1LL << 31) - 256)
+        return fail(SV_ERR_UNSUPPORTED, "sv_pack_verify: too many block positions");
+    if (!block_tokens || !ctx_lens || !qo_indptr || !tokens || !positions || !kv_lens)
+        return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: a required pointer is NULL");
+    if (!aligned(block_tokens, 4) || !aligned(ctx_lens, 4) || !aligned(qo_indptr, 4) || !aligned(tokens, 4) ||
+        !aligned(positions, 4) || !aligned(kv_lens, 4))
+        return fail(SV_ERR_INVALID_ARG, "sv_pack_verify: arrays must be 4-byte aligned");
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_pack_verify: injected launch failure");
+    return launched(sv::launch_pack(d, block_tokens, ctx_lens, qo_indptr, tokens, positions, kv_lens,
+                                    (hipStream_t)stream),
+                    "sv_pack_verify");
+}
+
+sv_status sv_append_kv(const sv_append_desc* desc, const void* k_new, const void* v_new,
+                       const int32_t* page_table, const int32_t* qo_indptr, const int32_t* ctx_lens,
+                       void* k_cache, void* v_cache, void* stream) {
+    if (!desc) return fail(SV_ERR_INVALID_ARG, "sv_append_kv: desc is NULL");
+    const sv_append_desc& d = *desc;
+    if (d.num_reqs < 1 || d.num_reqs > 65535)
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: num_reqs %d outside [1, 65535]", d.num_reqs);
+    if (d.block < 1 || d.block > SV_MAX_BLOCK)
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: block %d outside [1, %d]", d.block, SV_MAX_BLOCK);
+    if (d.total_max < 1 || d.num_kv_heads < 1 || d.num_kv_heads > 65535 || d.max_pages_per_req < 1 ||
+        d.num_pages < 1)
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: total_max, num_kv_heads, max_pages_per_req and num_pages "
+                                        "must be >= 1");
+    if (!is_pow2(d.page_size) || d.page_size > 4096)
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: page_size %d is not a power of two <= 4096", d.page_size);
+    if (d.dtype != SV_F32 && d.dtype != SV_BF16) return fail(SV_ERR_INVALID_ARG, "sv_append_kv: unknown dtype %d", d.dtype);
+    const long long row_bytes = (long long)d.head_dim * (d.dtype == SV_F32 ? 4 : 2);
+    if (d.head_dim < 1 || row_bytes % 16 != 0 || row_bytes > (1 << 16))
+        return fail(SV_ERR_UNSUPPORTED, "sv_append_kv: head_dim %d (the row must be a multiple of 16 bytes)",
+                    d.head_dim);
+    if ((long long)d.num_reqs * d.block > 0x7FFFFFFFLL)
+        return fail(SV_ERR_UNSUPPORTED, "sv_append_kv: too many block positions");
+    if (!k_new || !v_new || !page_table || !qo_indptr || !ctx_lens || !k_cache || !v_cache)
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: a required pointer is NULL");
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) ||
+        !aligned(page_table, 4) || !aligned(qo_indptr, 4) || !aligned(ctx_lens, 4))
+        return fail(SV_ERR_INVALID_ARG, "sv_append_kv: rows and caches must be 16-byte aligned, int32 arrays 4-byte "
+                                        "aligned");
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_append_kv: injected launch failure");
+    return launched(sv::launch_append(d, k_new, v_new, page_table, qo_indptr, ctx_lens, k_cache, v_cache,
+                                      (hipStream_t)stream),
+                    "sv_append_kv");
+}
+
 size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc) {
     if (check_accept(desc) != SV_OK) return 0;
     return sv::plan_accept(*desc).total;

@@ -48,4 +48,11 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const 
                          const float* u_accept, const float* u_sample, int32_t* accept_len,
                          int32_t* out_tokens, int32_t* flags, void* ws, hipStream_t stream);
 
+hipError_t launch_pack(const sv_pack_desc& d, const int32_t* block_tokens, const int32_t* ctx_lens,
+                       const int32_t* qo_indptr, int32_t* tokens, int32_t* positions, int32_t* kv_lens,
+                       hipStream_t stream);
+hipError_t launch_append(const sv_append_desc& d, const void* k_new, const void* v_new, const int32_t* page_table,
+                         const int32_t* qo_indptr, const int32_t* ctx_lens, void* k_cache, void* v_cache,
+                         hipStream_t stream);
+
 }  // namespace sv
