@@ -25,7 +25,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kThreads = 256;
-constexpr int kStatsLoads = 8;  // 16-byte loads in flight per thread in rowstats
+constexpr int kStatsLoads = 4;  // 16-byte loads in flight per thread in rowstats (16 KB chunks)
 constexpr int kResChunk = 8192;  // vocabulary chunk of the residual sums
 constexpr int kResPer = kResChunk / kThreads;  // tokens per thread in a chunk
 
@@ -60,6 +60,13 @@ __device__ inline float to_f(uint16_t h) { return bf2f(h); }
 
 template <typename T>
 __device__ inline float load_x(const T* row, int v) { return to_f(row[v]); }
+
+// 16-byte load with the non-temporal hint, for rows streamed once per pass (the
+// statistics and argmax passes): they would only evict reused lines from the caches
+template <typename V>
+__device__ inline V stream_load(const V* p) {
+    return __builtin_nontemporal_load(p);
+}
 
 // fp32 probability of token v of a row: softmax(l / T) from its (max, 1/sum) in logits
 // mode, the stored value in probability mode. Every kernel uses this one function.
@@ -127,7 +134,7 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
         const vec_t* rv = (const vec_t*)(row + beg);
 #pragma unroll
         for (int k = 0; k < kStatsLoads; k++) {
-            const vec_t v = rv[tid + k * kThreads];
+            const vec_t v = stream_load(rv + tid + k * kThreads);
 #pragma unroll
             for (int e = 0; e < VEC; e++) x[k * VEC + e] = to_f(v[e]) * a.invT;
         }
@@ -572,7 +579,7 @@ __global__ __launch_bounds__(kThreads) void argmax_kernel(AcceptArgs a) {
         const vec_t* rv = (const vec_t*)(row + beg);
         vec_t v[kStatsLoads];
 #pragma unroll
-        for (int k = 0; k < kStatsLoads; k++) v[k] = rv[tid + k * kThreads];
+        for (int k = 0; k < kStatsLoads; k++) v[k] = stream_load(rv + tid + k * kThreads);
 #pragma unroll
         for (int k = 0; k < kStatsLoads; k++)
 #pragma unroll
@@ -664,7 +671,7 @@ AcceptPlan plan_accept(const sv_accept_desc& d) {
     AcceptPlan p{};
     const int esz = d.dtype == SV_BF16 ? 2 : 4;
     const int vec = 16 / esz;
-    p.stats_chunk = kThreads * kStatsLoads * vec;  // 32 KB of logits per workgroup
+    p.stats_chunk = kThreads * kStatsLoads * vec;  // 16 KB of logits per workgroup
     p.stats_chunks = (d.vocab + p.stats_chunk - 1) / p.stats_chunk;
     p.res_chunk = kResChunk;
     p.res_chunks = (d.vocab + p.res_chunk - 1) / p.res_chunk;

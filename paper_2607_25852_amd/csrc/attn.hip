@@ -82,14 +82,16 @@ struct LdsRing {
 
 // Asynchronous 16-byte-per-lane copy global -> LDS: lane l's 16 bytes land at
 // lds_base + 16*l. Issued from inline assembly so the compiler does not drain it
-// before every LDS read; completion is awaited explicitly with wait_vm<N>().
+// before every LDS read; completion is awaited explicitly with wait_vm<N>(). The
+// loads carry the non-temporal hint: every K/V byte is read by one workgroup once,
+// so keeping it in L2 and the last-level cache only evicts lines that are reused.
 __device__ inline void dma16(const void* gptr, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base)
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(gptr), "s"(lds_base)
                  : "memory", "m0");
 }
 // Same copy with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane byte offset.
 __device__ inline void dma16s(uint32_t voff, const void* sbase, uint32_t lds_base) {
-    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase),
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 nt" ::"v"(voff), "s"(sbase),
                  "s"(lds_base)
                  : "memory", "m0");
 }
