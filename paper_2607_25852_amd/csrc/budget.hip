@@ -14,7 +14,7 @@
 namespace sv {
 namespace {
 
-constexpr int kThreads = 1024;
+constexpr int kThreads = 512;
 constexpr int kMaxKeys = SV_MAX_BUDGET_POSITIONS;
 constexpr int kMaxReqs = SV_MAX_BUDGET_REQS;
 
@@ -99,7 +99,9 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
 
     // 2. bitonic sort, descending, of NPAD keys
     int buf = 1;
+#pragma unroll
     for (int k = 2; k <= NPAD; k <<= 1) {
+#pragma unroll
         for (int j = k >> 1; j > 0; j >>= 1) {
             if (j < KPT) {
 #pragma unroll
@@ -182,7 +184,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
     __syncthreads();
 
     // 6. keep = count - 1; qo_indptr = exclusive scan of the counts (block scan)
-    constexpr int kPer = kMaxReqs / kThreads;  // 4 requests per thread
+    constexpr int kPer = kMaxReqs / kThreads;  // 8 requests per thread
     int loc[kPer];
     int rsum = 0;
     for (int e = 0; e < kPer; e++) {
@@ -236,7 +238,8 @@ hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* ke
     if (kpt <= 1) SV_LAUNCH_BUDGET(1);
     else if (kpt <= 2) SV_LAUNCH_BUDGET(2);
     else if (kpt <= 4) SV_LAUNCH_BUDGET(4);
-    else SV_LAUNCH_BUDGET(8);
+    else if (kpt <= 8) SV_LAUNCH_BUDGET(8);
+    else SV_LAUNCH_BUDGET(16);
 #undef SV_LAUNCH_BUDGET
     return hipGetLastError();
 }
