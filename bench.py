@@ -344,6 +344,29 @@ def main():
     assert np.array_equal(p_kvl.cpu().numpy(), rnd.kv_lens_host)
     ap_bytes = 4.0 * rnd.K * cfg.Hkv * cfg.d * e_sz
 
+    # the drafter's side: softmax statistics and confidences of every draft row, then the
+    # acceptance that takes the draft rows' statistics instead of re-reading them (same
+    # outputs bit for bit), both on the same round and outside the timed steps
+    dsdesc = binding.draft_stats_desc(cfg.R, cfg.b - 1, cfg.V, binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
+    ds_ws = torch.empty(max(binding.draft_stats_workspace_size(dsdesc), 256), dtype=torch.uint8, device="cuda")
+    ds_stats = torch.empty((cfg.R * (cfg.b - 1), 2), dtype=torch.float32, device="cuda")
+    ds_conf = torch.empty(cfg.R * (cfg.b - 1), dtype=torch.float32, device="cuda")
+
+    def dstats():
+        binding.draft_stats(dsdesc, rnd.draft, ds_stats, ds_conf, ds_ws)
+
+    def accept_with_stats():
+        binding.spec_accept_stats(rnd.xdesc, rnd.target, rnd.draft, ds_stats, rnd.tokens, rnd.qo, rnd.u_accept,
+                                  rnd.u_sample, rnd.accept_len, rnd.out_tokens, rnd.flags, rnd.acc_ws)
+
+    t_dstats = time_loop(torch, stream, dstats, args.steps)
+    ds_bytes = float(cfg.R * (cfg.b - 1)) * cfg.V * e_sz
+    rnd.run_accept()
+    ref_out = (rnd.accept_len.clone(), rnd.out_tokens.clone())
+    t_acc_stats = time_loop(torch, stream, accept_with_stats, args.steps)
+    assert torch.equal(rnd.accept_len, ref_out[0]) and torch.equal(rnd.out_tokens, ref_out[1])
+    xs_bytes = float(rnd.K) * cfg.V * e_sz
+
     if args.copy_probe:
         log("copy probe")
         copy_probe()
@@ -384,7 +407,12 @@ def main():
                     "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
                     "greedy_acceptance_algorithmic_bytes": g_bytes,
                     "pack_us": t_pack * 1e3, "append_us": t_append * 1e3,
-                    "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes},
+                    "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes,
+                    "draft_stats_us": t_dstats * 1e3, "draft_stats_gbs": ds_bytes / (t_dstats * 1e-3) / 1e9,
+                    "draft_stats_algorithmic_bytes": ds_bytes,
+                    "acceptance_with_draft_stats_us": t_acc_stats * 1e3,
+                    "acceptance_with_draft_stats_gbs": xs_bytes / (t_acc_stats * 1e-3) / 1e9,
+                    "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
         "cpu_baseline": cpu,
     }

@@ -21,6 +21,10 @@
  *                    cut, and the extra token drawn from the normalised residual
  *                    max(p - q, 0), or from p when the whole block survives.
  *
+ * On the drafter's side, sv_draft_stats gives each draft row its softmax
+ * normaliser and the confidence c_t the budget takes; sv_spec_accept_stats is the
+ * acceptance that uses those normalisers instead of re-reading the draft rows.
+ *
  * Conventions shared by every entry point
  *   - All array pointers are caller-owned DEVICE memory unless marked "host".
  *     The library allocates nothing and keeps no state between calls; each call
@@ -276,6 +280,49 @@ sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const v
                          int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
                          void* stream);
 size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc);
+
+/*
+ * sv_spec_accept_stats -- sv_spec_accept (LOGITS, temperature > 0) with the draft rows'
+ * softmax statistics supplied by the drafter (sv_draft_stats, same temperature and
+ * dtype): draft_stats [R, b-1, 2] fp32 holds (m, S) per draft row, m = max_v l(v)/T and
+ * S = sum_v 2^((l(v)/T - m) log2 e). The draft rows are then read only at the drafted
+ * token and, after a rejection, the one residual row; the kept target rows are still
+ * streamed once. With statistics from sv_draft_stats the results equal those of
+ * sv_spec_accept bit for bit (the same chunks and the same merge). The confidence
+ * c_t of the budget is the same pass's max_v Q_t(v) (Sec. 4.2), so the drafter's one
+ * pass over its rows serves both. Other arguments, workspace and errors as
+ * sv_spec_accept; draft_stats is device memory, 8-byte aligned, NULL only when b == 1.
+ */
+sv_status sv_spec_accept_stats(const sv_accept_desc* desc, const void* target, const void* draft,
+                               const float* draft_stats, const int32_t* draft_tokens, const int32_t* qo_indptr,
+                               const float* u_accept, const float* u_sample, int32_t* accept_len,
+                               int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------- */
+/* Draft-row statistics (the drafter's side of the round: the confidences c_t */
+/* of Sec. 4.2 and the normalisers acceptance needs)                          */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t num_reqs;   /* R >= 1                                   */
+    int32_t drafts;     /* rows per request (b - 1 of the round) >= 1 */
+    int32_t vocab;      /* V in [1, 2^22]                           */
+    int32_t dtype;      /* sv_dtype of the logits                   */
+    float temperature;  /* T > 0, as in the acceptance call          */
+} sv_draft_stats_desc;
+
+/*
+ * sv_draft_stats -- for every draft row r of draft_logits [R, drafts, V]:
+ *   stats[r] = (m, S), m = max_v l(v)/T, S = sum_v 2^((l(v)/T - m) log2 e) (fp32, in
+ *   the chunks and merge order of sv_spec_accept);
+ *   conf[r] = max_v softmax(l/T)(v) = 1/S (0 for a row without a finite entry), the
+ *   token-level confidence c_t of Sec. 4.2 that sv_alloc_budget takes.
+ * stats [R*drafts, 2] fp32 out (8-byte aligned); conf [R*drafts] fp32 out or NULL;
+ * ws scratch of sv_draft_stats_workspace_size(desc) bytes, overwritten. Device memory
+ * owned by the caller; asynchronous on `stream`; the library allocates nothing.
+ */
+size_t sv_draft_stats_workspace_size(const sv_draft_stats_desc* desc);
+sv_status sv_draft_stats(const sv_draft_stats_desc* desc, const void* draft_logits, float* stats, float* conf,
+                         void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------- */
 /* status                                                                      */

@@ -255,3 +255,20 @@ def append_kv(k_new, v_new, page_table, qo_indptr, ctx_lens, k_cache, v_cache, b
             kc[pg, :, s % P, :] = k_new[qo[i] + j]
             vc[pg, :, s % P, :] = v_new[qo[i] + j]
     return kc, vc
+
+
+# ------------------------------------------------------------------------------------
+# draft-row statistics (the confidence c_t of Sec. 4.2 and the draft softmax normaliser)
+# ------------------------------------------------------------------------------------
+def draft_stats(draft_logits, temperature=1.0, dtype="f32"):
+    """For every draft row (last axis = vocabulary) of the stored logits l (fp32, or
+    uint16 bf16 bits when dtype="bf16"), in fp64: m = max_v l(v)/T,
+    S = sum_v exp(l(v)/T - m), conf = max_v softmax(l/T)(v) = 1/S.
+    Returns dict(m, S, conf) shaped like the rows."""
+    x = np.asarray(draft_logits)
+    if dtype == "bf16":
+        x = (x.astype(np.uint32) << 16).view(np.float32)
+    z = x.astype(np.float64) / float(np.float32(temperature))
+    m = z.max(axis=-1)
+    S = np.exp(z - m[..., None]).sum(axis=-1)
+    return dict(m=m, S=S, conf=1.0 / S)

@@ -22,8 +22,8 @@ SV_MAX_RATIOS = 8
 
 # every symbol the header declares (checked by the ABI test)
 EXPORTED = ("sv_alloc_budget", "sv_pack_verify", "sv_append_kv", "sv_verify_attn", "sv_verify_attn_workspace_size",
-            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_status_string", "sv_last_error",
-            "sv_abi_version")
+            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_stats", "sv_draft_stats",
+            "sv_draft_stats_workspace_size", "sv_status_string", "sv_last_error", "sv_abi_version")
 
 
 class BudgetDesc(ctypes.Structure):
@@ -45,6 +45,11 @@ class AttnDesc(ctypes.Structure):
 class AcceptDesc(ctypes.Structure):
     _fields_ = [("num_reqs", ctypes.c_int32), ("block", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("temperature", ctypes.c_float)]
+
+
+class DraftStatsDesc(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("drafts", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("temperature", ctypes.c_float)]
 
 
 class PackDesc(ctypes.Structure):
@@ -87,6 +92,13 @@ def load() -> ctypes.CDLL:
     lib.sv_spec_accept.restype = i32
     lib.sv_spec_accept_workspace_size.argtypes = [ctypes.POINTER(AcceptDesc)]
     lib.sv_spec_accept_workspace_size.restype = ctypes.c_size_t
+    lib.sv_spec_accept_stats.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P, P,
+                                         ctypes.c_size_t, P]
+    lib.sv_spec_accept_stats.restype = i32
+    lib.sv_draft_stats.argtypes = [ctypes.POINTER(DraftStatsDesc), P, P, P, P, ctypes.c_size_t, P]
+    lib.sv_draft_stats.restype = i32
+    lib.sv_draft_stats_workspace_size.argtypes = [ctypes.POINTER(DraftStatsDesc)]
+    lib.sv_draft_stats_workspace_size.restype = ctypes.c_size_t
     lib.sv_pack_verify.argtypes = [ctypes.POINTER(PackDesc), P, P, P, P, P, P, P]
     lib.sv_pack_verify.restype = i32
     lib.sv_append_kv.argtypes = [ctypes.POINTER(AppendDesc), P, P, P, P, P, P, P, P]
@@ -242,4 +254,34 @@ def spec_accept(desc: AcceptDesc, target, draft, draft_tokens, qo_indptr, u_acce
     st = load().sv_spec_accept(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_tokens),
                                _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample), _ptr(accept_len),
                                _ptr(out_tokens), _ptr(flags), _ptr(ws), nbytes, _stream(stream))
+    _check(st)
+
+
+# ------------------------------------------------------------------------------------
+# sv_spec_accept_stats, sv_draft_stats
+# ------------------------------------------------------------------------------------
+def spec_accept_stats(desc: AcceptDesc, target, draft, draft_stats, draft_tokens, qo_indptr, u_accept, u_sample,
+                      accept_len, out_tokens, flags=None, ws=None, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().sv_spec_accept_stats(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_stats),
+                                     _ptr(draft_tokens), _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample),
+                                     _ptr(accept_len), _ptr(out_tokens), _ptr(flags), _ptr(ws), nbytes,
+                                     _stream(stream))
+    _check(st)
+
+
+def draft_stats_desc(R: int, drafts: int, V: int, dtype: int, temperature: float = 1.0) -> DraftStatsDesc:
+    d = DraftStatsDesc()
+    d.num_reqs, d.drafts, d.vocab, d.dtype, d.temperature = R, drafts, V, dtype, temperature
+    return d
+
+
+def draft_stats_workspace_size(desc: DraftStatsDesc) -> int:
+    return int(load().sv_draft_stats_workspace_size(ctypes.byref(desc)))
+
+
+def draft_stats(desc: DraftStatsDesc, draft_logits, stats, conf=None, ws=None, stream=None):
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().sv_draft_stats(ctypes.byref(desc), _ptr(draft_logits), _ptr(stats), _ptr(conf), _ptr(ws), nbytes,
+                               _stream(stream))
     _check(st)

@@ -45,6 +45,7 @@ struct AcceptArgs {
     int32_t* accept_len;
     int32_t* out_tokens;
     int32_t* flags;
+    const float2* dstats;  // [R*D] (max, sum) of the draft rows from the drafter, or NULL
     float2* stats_t;  // [R*b][NC]
     float2* stats_q;  // [R*D][NC]
     ReqPlan* plan;    // [R]
@@ -98,45 +99,24 @@ __device__ inline const T* row_ptr(const void* base, long long row, int V) {
     return (const T*)base + row * (long long)V;
 }
 
-// ----------------------------------------------------------------------------------
-// rowstats: flat grid of (row slot, chunk), R*b + R*D slots of NC chunks
-// ----------------------------------------------------------------------------------
+// (max, sum of 2^((x - max) log2e)) of x = l * invT over the chunk [beg, end) of one row,
+// valid in thread 0: every 16-byte load of the chunk is issued before any arithmetic
 template <typename T>
-__global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
+__device__ inline float2 chunk_stats(const T* row, int beg, int end, int V, int stats_chunk, float invT,
+                                     float* red) {
     constexpr int VEC = 16 / sizeof(T);
     typedef T vec_t __attribute__((ext_vector_type(VEC)));
-    __shared__ float red[kThreads / 64];
-
-    const int slot = blockIdx.x / a.NC, c = blockIdx.x % a.NC;  // flat grid: (row slot, chunk)
-    const int RB = a.R * a.b;
-    const T* row;
-    float2* dst;
-    if (slot < RB) {
-        const int K = a.qo[a.R];
-        if (slot >= K) return;
-        row = row_ptr<T>(a.target, slot, a.V);
-        dst = a.stats_t + (size_t)slot * a.NC;
-    } else {
-        const int s2 = slot - RB;
-        const int i = s2 / a.D, t = s2 % a.D;
-        const int n = a.qo[i + 1] - a.qo[i] - 1;
-        if (t >= n) return;
-        row = row_ptr<T>(a.draft, (long long)i * a.D + t, a.V);
-        dst = a.stats_q + (size_t)(i * a.D + t) * a.NC;
-    }
-    const int beg = c * a.stats_chunk;
-    const int end = min(a.V, beg + a.stats_chunk);
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
 
     float x[kStatsLoads * VEC];
-    const bool vec_ok = (a.V % VEC) == 0 && (end - beg) == a.stats_chunk;
+    const bool vec_ok = (V % VEC) == 0 && (end - beg) == stats_chunk;
     if (vec_ok) {
         const vec_t* rv = (const vec_t*)(row + beg);
 #pragma unroll
         for (int k = 0; k < kStatsLoads; k++) {
             const vec_t v = stream_load(rv + tid + k * kThreads);
 #pragma unroll
-            for (int e = 0; e < VEC; e++) x[k * VEC + e] = to_f(v[e]) * a.invT;
+            for (int e = 0; e < VEC; e++) x[k * VEC + e] = to_f(v[e]) * invT;
         }
     } else {
 #pragma unroll
@@ -144,7 +124,7 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
 #pragma unroll
             for (int e = 0; e < VEC; e++) {
                 const int v = beg + (tid + k * kThreads) * VEC + e;
-                x[k * VEC + e] = v < end ? load_x<T>(row, v) * a.invT : -INFINITY;
+                x[k * VEC + e] = v < end ? load_x<T>(row, v) * invT : -INFINITY;
             }
     }
     float mx = -INFINITY;
@@ -165,16 +145,44 @@ __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
     for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
     if (lane == 0) red[w] = s;
     __syncthreads();
-    if (tid == 0) {
-        float tot = 0.0f;
+    float tot = 0.0f;
+    if (tid == 0)
         for (int k = 0; k < kThreads / 64; k++) tot += red[k];
-        dst[c] = make_float2(mx, tot);
+    return make_float2(mx, tot);
+}
+
+// ----------------------------------------------------------------------------------
+// rowstats: flat grid of (row slot, chunk), R*b + R*D slots of NC chunks (R*b when the
+// draft rows' statistics are given)
+// ----------------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
+    __shared__ float red[kThreads / 64];
+    const int slot = blockIdx.x / a.NC, c = blockIdx.x % a.NC;  // flat grid: (row slot, chunk)
+    const int RB = a.R * a.b;
+    const T* row;
+    float2* dst;
+    if (slot < RB) {
+        const int K = a.qo[a.R];
+        if (slot >= K) return;
+        row = row_ptr<T>(a.target, slot, a.V);
+        dst = a.stats_t + (size_t)slot * a.NC;
+    } else {
+        const int s2 = slot - RB;
+        const int i = s2 / a.D, t = s2 % a.D;
+        const int n = a.qo[i + 1] - a.qo[i] - 1;
+        if (t >= n) return;
+        row = row_ptr<T>(a.draft, (long long)i * a.D + t, a.V);
+        dst = a.stats_q + (size_t)(i * a.D + t) * a.NC;
     }
+    const int beg = c * a.stats_chunk;
+    const float2 st = chunk_stats<T>(row, beg, min(a.V, beg + a.stats_chunk), a.V, a.stats_chunk, a.invT, red);
+    if (threadIdx.x == 0) dst[c] = st;
 }
 
 // combine the per-chunk (max, sum) of one row; chunk statistics are loaded 8 at a time
 // so their latencies overlap
-__device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS) {
+__device__ inline void merge_stats_ms(const float2* st, int NC, float& m, float& Sum) {
     float mm = -INFINITY, S = 0.0f;
     for (int c0 = 0; c0 < NC; c0 += 8) {
         float2 v[8];
@@ -194,7 +202,16 @@ __device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS
         }
     }
     m = mm;
-    iS = S > 0.0f ? 1.0f / S : 0.0f;
+    Sum = S;
+}
+
+__device__ inline float inv_sum(float S) { return S > 0.0f ? 1.0f / S : 0.0f; }
+
+// (max, 1/sum) of one row from its chunk statistics
+__device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS) {
+    float S;
+    merge_stats_ms(st, NC, m, S);
+    iS = inv_sum(S);
 }
 
 // ----------------------------------------------------------------------------------
@@ -222,7 +239,15 @@ __global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
     float m = 0.0f, iS = 0.0f;
     if (LOGITS) {
         if (lane <= n) merge_stats(a.stats_t + (size_t)(q0 + lane) * a.NC, a.NC, m, iS);
-        else if (lane >= 32 && lane - 32 < n) merge_stats(a.stats_q + (size_t)(i * a.D + lane - 32) * a.NC, a.NC, m, iS);
+        else if (lane >= 32 && lane - 32 < n) {
+            if (a.dstats) {  // the drafter's own (max, sum) of this row
+                const float2 st = a.dstats[(size_t)i * a.D + lane - 32];
+                m = st.x;
+                iS = inv_sum(st.y);
+            } else {
+                merge_stats(a.stats_q + (size_t)(i * a.D + lane - 32) * a.NC, a.NC, m, iS);
+            }
+        }
     }
     // the test of draft t+1 in lane t: P_t(d) vs u * Q_{t+1}(d)
     const float mPt = __shfl(m, lane & 31, 64), iSPt = __shfl(iS, lane & 31, 64);
@@ -531,6 +556,39 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
 }
 
 // ----------------------------------------------------------------------------------
+// Draft-row statistics (the drafter's side of the round): per draft row the softmax
+// (max, sum) that acceptance would compute itself -- the same chunks, the same merge --
+// and the confidence max_v Q_t(v) = 1 / sum that the budget takes as c_t.
+// ----------------------------------------------------------------------------------
+struct DStatsArgs {
+    const void* logits;  // [rows, V]
+    float2* part;        // [rows][NC]
+    float2* stats;       // [rows] (max, sum)
+    float* conf;         // [rows] or NULL
+    int rows, V, NC, stats_chunk;
+    float invT;
+};
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void dstats_chunk_kernel(DStatsArgs a) {
+    __shared__ float red[kThreads / 64];
+    const int r = blockIdx.x / a.NC, c = blockIdx.x % a.NC;
+    const T* row = row_ptr<T>(a.logits, r, a.V);
+    const int beg = c * a.stats_chunk;
+    const float2 st = chunk_stats<T>(row, beg, min(a.V, beg + a.stats_chunk), a.V, a.stats_chunk, a.invT, red);
+    if (threadIdx.x == 0) a.part[(size_t)r * a.NC + c] = st;
+}
+
+__global__ __launch_bounds__(256) void dstats_merge_kernel(DStatsArgs a) {
+    const int r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= a.rows) return;
+    float m, S;
+    merge_stats_ms(a.part + (size_t)r * a.NC, a.NC, m, S);
+    a.stats[r] = make_float2(m, S);
+    if (a.conf) a.conf[r] = inv_sum(S);  // max_v of exp(x - m) / S is exp(0) / S
+}
+
+// ----------------------------------------------------------------------------------
 // Greedy verification (temperature 0): rejection sampling with one-hot target and draft
 // rows. Draft t is accepted iff it is the argmax of P_{t-1}; the extra token is the argmax
 // of P_a. Argmax: largest stored value (lowest index on ties, NaN skipped), so only the
@@ -691,9 +749,10 @@ AcceptPlan plan_accept(const sv_accept_desc& d) {
 }
 
 hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const void* target,
-                         const void* draft, const int32_t* draft_tokens, const int32_t* qo_indptr,
-                         const float* u_accept, const float* u_sample, int32_t* accept_len,
-                         int32_t* out_tokens, int32_t* flags, void* ws, hipStream_t stream) {
+                         const void* draft, const float* draft_stats, const int32_t* draft_tokens,
+                         const int32_t* qo_indptr, const float* u_accept, const float* u_sample,
+                         int32_t* accept_len, int32_t* out_tokens, int32_t* flags, void* ws,
+                         hipStream_t stream) {
     AcceptArgs a{};
     a.target = target;
     a.draft = draft;
@@ -704,6 +763,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     a.accept_len = accept_len;
     a.out_tokens = out_tokens;
     a.flags = flags;
+    a.dstats = (const float2*)draft_stats;
     char* w = (char*)ws;
     a.stats_t = (float2*)(w + p.off_stats_t);
     a.stats_q = (float2*)(w + p.off_stats_q);
@@ -728,7 +788,8 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         return hipGetLastError();
     }
     if (logits) {
-        const long long slots = (long long)d.num_reqs * d.block + (long long)d.num_reqs * (d.block > 1 ? d.block - 1 : 0);
+        const long long slots = (long long)d.num_reqs * d.block +
+                                (draft_stats ? 0LL : (long long)d.num_reqs * (d.block > 1 ? d.block - 1 : 0));
         const dim3 g((unsigned)(slots * p.stats_chunks));
         if (bf) hipLaunchKernelGGL(rowstats_kernel<uint16_t>, g, dim3(kThreads), 0, stream, a);
         else hipLaunchKernelGGL(rowstats_kernel<float>, g, dim3(kThreads), 0, stream, a);
@@ -748,6 +809,35 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         SV_ACCEPT_PHASES(false, float);
     }
 #undef SV_ACCEPT_PHASES
+    return hipGetLastError();
+}
+
+size_t draft_stats_workspace(const sv_draft_stats_desc& d) {
+    const int esz = d.dtype == SV_BF16 ? 2 : 4;
+    const int chunk = kThreads * kStatsLoads * (16 / esz);
+    const size_t nc = ((size_t)d.vocab + chunk - 1) / chunk;
+    return (size_t)d.num_reqs * d.drafts * nc * sizeof(float2);
+}
+
+hipError_t launch_draft_stats(const sv_draft_stats_desc& d, const void* logits, float* stats, float* conf, void* ws,
+                              hipStream_t stream) {
+    DStatsArgs a{};
+    const int esz = d.dtype == SV_BF16 ? 2 : 4;
+    a.logits = logits;
+    a.part = (float2*)ws;
+    a.stats = (float2*)stats;
+    a.conf = conf;
+    a.rows = d.num_reqs * d.drafts;
+    a.V = d.vocab;
+    a.stats_chunk = kThreads * kStatsLoads * (16 / esz);  // the chunks of sv_spec_accept
+    a.NC = (d.vocab + a.stats_chunk - 1) / a.stats_chunk;
+    a.invT = 1.0f / d.temperature;
+    const dim3 g((unsigned)((long long)a.rows * a.NC));
+    if (d.dtype == SV_BF16) hipLaunchKernelGGL(dstats_chunk_kernel<uint16_t>, g, dim3(kThreads), 0, stream, a);
+    else hipLaunchKernelGGL(dstats_chunk_kernel<float>, g, dim3(kThreads), 0, stream, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(dstats_merge_kernel, dim3((unsigned)((a.rows + 255) / 256)), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -245,31 +245,104 @@ size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc) {
     return sv::plan_accept(*desc).total;
 }
 
-sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const void* draft,
-                         const int32_t* draft_tokens, const int32_t* qo_indptr,
-                         const float* u_accept, const float* u_sample, int32_t* accept_len,
-                         int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
-                         void* stream) {
+}  // extern "C"
+
+namespace {
+
+sv_status spec_accept(const char* name, const sv_accept_desc* desc, const void* target, const void* draft,
+                      const float* draft_stats, const int32_t* draft_tokens, const int32_t* qo_indptr,
+                      const float* u_accept, const float* u_sample, int32_t* accept_len, int32_t* out_tokens,
+                      int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
     sv_status st = check_accept(desc);
     if (st != SV_OK) return st;
     const bool has_drafts = desc->block > 1;
     const bool greedy = desc->temperature == 0.0f;  // reads neither draft rows nor uniforms
     if (!target || !qo_indptr || !accept_len || !out_tokens || (has_drafts && !draft_tokens) ||
         (!greedy && (!u_sample || (has_drafts && (!draft || !u_accept)))))
-        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept: a required pointer is NULL");
+        return fail(SV_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
     if (!aligned(target, 16) || !aligned(draft, 16) || !aligned(ws, 16) || !aligned(draft_tokens, 4) ||
         !aligned(qo_indptr, 4) || !aligned(u_accept, 4) || !aligned(u_sample, 4) || !aligned(accept_len, 4) ||
-        !aligned(out_tokens, 4) || !aligned(flags, 4))
+        !aligned(out_tokens, 4) || !aligned(flags, 4) || !aligned(draft_stats, 8))
         return fail(SV_ERR_INVALID_ARG,
-                    "sv_spec_accept: target, draft and ws must be 16-byte aligned, int32/fp32 arrays 4-byte aligned");
+                    "%s: target, draft and ws must be 16-byte aligned, draft_stats 8-byte aligned, int32/fp32 "
+                    "arrays 4-byte aligned",
+                    name);
     const sv::AcceptPlan p = sv::plan_accept(*desc);
     if (!ws || ws_bytes < p.total)
-        return fail(SV_ERR_WORKSPACE, "sv_spec_accept: workspace of %zu bytes needed, %zu given", p.total,
+        return fail(SV_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name, p.total,
                     ws ? ws_bytes : (size_t)0);
-    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_spec_accept: injected launch failure");
-    return launched(sv::launch_accept(*desc, p, target, draft, draft_tokens, qo_indptr, u_accept, u_sample,
-                                      accept_len, out_tokens, flags, ws, (hipStream_t)stream),
-                    "sv_spec_accept");
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "%s: injected launch failure", name);
+    return launched(sv::launch_accept(*desc, p, target, draft, draft_stats, draft_tokens, qo_indptr, u_accept,
+                                      u_sample, accept_len, out_tokens, flags, ws, (hipStream_t)stream),
+                    name);
+}
+
+sv_status check_draft_stats(const sv_draft_stats_desc* d) {
+    if (!d) return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: desc is NULL");
+    if (d->num_reqs < 1 || d->drafts < 1)
+        return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: num_reqs %d and drafts %d must be >= 1", d->num_reqs,
+                    d->drafts);
+    if (d->vocab < 1 || d->vocab > SV_MAX_VOCAB)
+        return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: vocab %d outside [1, %d]", d->vocab, SV_MAX_VOCAB);
+    if (d->dtype != SV_F32 && d->dtype != SV_BF16)
+        return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: unknown dtype %d", d->dtype);
+    if (!(d->temperature > 0.0f) || std::isinf(d->temperature))
+        return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: temperature must be finite and > 0");
+    const long long rows = (long long)d->num_reqs * d->drafts;
+    const int chunk = 256 * 4 * (d->dtype == SV_BF16 ? 8 : 4);  // the statistics chunk of sv_spec_accept
+    const long long nc = ((long long)d->vocab + chunk - 1) / chunk;
+    if (rows > (1LL << 30) || rows * nc * 256 > 0xFFFFFFFFLL)
+        return fail(SV_ERR_UNSUPPORTED, "sv_draft_stats: %lld rows x vocab %d exceed one launch", rows, d->vocab);
+    return SV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const void* draft,
+                         const int32_t* draft_tokens, const int32_t* qo_indptr,
+                         const float* u_accept, const float* u_sample, int32_t* accept_len,
+                         int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
+                         void* stream) {
+    return spec_accept("sv_spec_accept", desc, target, draft, nullptr, draft_tokens, qo_indptr, u_accept, u_sample,
+                       accept_len, out_tokens, flags, ws, ws_bytes, stream);
+}
+
+sv_status sv_spec_accept_stats(const sv_accept_desc* desc, const void* target, const void* draft,
+                               const float* draft_stats, const int32_t* draft_tokens, const int32_t* qo_indptr,
+                               const float* u_accept, const float* u_sample, int32_t* accept_len,
+                               int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+    if (desc && (desc->kind != SV_LOGITS || !(desc->temperature > 0.0f)))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_spec_accept_stats: draft statistics apply to rejection sampling (LOGITS, temperature > 0)");
+    if (desc && desc->block > 1 && !draft_stats)
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept_stats: draft_stats is NULL");
+    return spec_accept("sv_spec_accept_stats", desc, target, draft, desc && desc->block > 1 ? draft_stats : nullptr,
+                       draft_tokens, qo_indptr, u_accept, u_sample, accept_len, out_tokens, flags, ws, ws_bytes,
+                       stream);
+}
+
+size_t sv_draft_stats_workspace_size(const sv_draft_stats_desc* desc) {
+    if (check_draft_stats(desc) != SV_OK) return 0;
+    return sv::draft_stats_workspace(*desc);
+}
+
+sv_status sv_draft_stats(const sv_draft_stats_desc* desc, const void* draft_logits, float* stats, float* conf,
+                         void* ws, size_t ws_bytes, void* stream) {
+    sv_status st = check_draft_stats(desc);
+    if (st != SV_OK) return st;
+    if (!draft_logits || !stats) return fail(SV_ERR_INVALID_ARG, "sv_draft_stats: a required pointer is NULL");
+    if (!aligned(draft_logits, 16) || !aligned(stats, 8) || !aligned(conf, 4) || !aligned(ws, 16))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_draft_stats: logits and ws must be 16-byte aligned, stats 8-byte, conf 4-byte aligned");
+    const size_t need = sv::draft_stats_workspace(*desc);
+    if (!ws || ws_bytes < need)
+        return fail(SV_ERR_WORKSPACE, "sv_draft_stats: workspace of %zu bytes needed, %zu given", need,
+                    ws ? ws_bytes : (size_t)0);
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_draft_stats: injected launch failure");
+    return launched(sv::launch_draft_stats(*desc, draft_logits, stats, conf, ws, (hipStream_t)stream),
+                    "sv_draft_stats");
 }
 
 const char* sv_status_string(int32_t status) {

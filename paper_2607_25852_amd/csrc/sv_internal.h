@@ -44,9 +44,13 @@ struct AcceptPlan {
 };
 AcceptPlan plan_accept(const sv_accept_desc& d);
 hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const void* target,
-                         const void* draft, const int32_t* draft_tokens, const int32_t* qo_indptr,
-                         const float* u_accept, const float* u_sample, int32_t* accept_len,
-                         int32_t* out_tokens, int32_t* flags, void* ws, hipStream_t stream);
+                         const void* draft, const float* draft_stats, const int32_t* draft_tokens,
+                         const int32_t* qo_indptr, const float* u_accept, const float* u_sample,
+                         int32_t* accept_len, int32_t* out_tokens, int32_t* flags, void* ws,
+                         hipStream_t stream);
+size_t draft_stats_workspace(const sv_draft_stats_desc& d);
+hipError_t launch_draft_stats(const sv_draft_stats_desc& d, const void* logits, float* stats, float* conf, void* ws,
+                              hipStream_t stream);
 
 hipError_t launch_pack(const sv_pack_desc& d, const int32_t* block_tokens, const int32_t* ctx_lens,
                        const int32_t* qo_indptr, int32_t* tokens, int32_t* positions, int32_t* kv_lens,

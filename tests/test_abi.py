@@ -186,3 +186,62 @@ def test_misaligned_pointers_are_rejected(lib):
     st = lib.sv_spec_accept(ctypes.byref(d), ctypes.c_void_p(4096 + 8), ok16, ok16, ok16, ok16, ok16, ok16, ok16,
                             None, ok16, need, None)
     assert st == B.SV_ERR_INVALID_ARG and "aligned" in B.last_error()
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(R=0), 1, "num_reqs"),
+    (dict(drafts=0), 1, "drafts"),
+    (dict(V=0), 1, "vocab"),
+    (dict(V=(1 << 22) + 1), 1, "vocab"),
+    (dict(dtype=7), 1, "dtype"),
+    (dict(temperature=0.0), 1, "temperature"),
+    (dict(temperature=float("nan")), 1, "temperature"),
+    (dict(temperature=float("inf")), 1, "temperature"),
+])
+def test_draft_stats_descriptor_checks(lib, kw, status, msg):
+    base = dict(R=8, drafts=15, V=32768, dtype=B.SV_BF16, temperature=1.0)
+    base.update(kw)
+    d = B.draft_stats_desc(base["R"], base["drafts"], base["V"], base["dtype"], base["temperature"])
+    assert lib.sv_draft_stats_workspace_size(ctypes.byref(d)) == 0
+    assert lib.sv_draft_stats(ctypes.byref(d), None, None, None, None, 0, None) == status
+    assert msg in B.last_error()
+
+
+def test_draft_stats_pointer_workspace_and_fault_checks(lib, monkeypatch):
+    """NULL, misaligned and short-workspace calls are rejected on the host; with
+    SV_FAULT_INJECT=launch a valid call reports SV_ERR_HIP without launching (the fake
+    addresses are never touched)."""
+    ok16, odd = ctypes.c_void_p(4096), ctypes.c_void_p(4096 + 4)
+    d = B.draft_stats_desc(4, 7, 1000, B.SV_F32, 0.7)
+    need = lib.sv_draft_stats_workspace_size(ctypes.byref(d))
+    assert need == 4 * 7 * 1 * 8  # one 16 KB chunk of fp32 logits per row, a float2 each
+    assert lib.sv_draft_stats(ctypes.byref(d), None, ok16, None, ok16, need, None) == 1
+    assert "NULL" in B.last_error()
+    assert lib.sv_draft_stats(ctypes.byref(d), ok16, odd, None, ok16, need, None) == 1
+    assert "aligned" in B.last_error()
+    assert lib.sv_draft_stats(ctypes.byref(d), ok16, ok16, None, ok16, need - 1, None) == B.SV_ERR_WORKSPACE
+    monkeypatch.setenv("SV_FAULT_INJECT", "launch")
+    assert lib.sv_draft_stats(ctypes.byref(d), ok16, ok16, ok16, ok16, need, None) == B.SV_ERR_HIP
+
+
+def test_accept_stats_checks(lib, monkeypatch):
+    """sv_spec_accept_stats: logits mode with T > 0 only, draft_stats required when b > 1,
+    8-byte aligned; otherwise the checks of sv_spec_accept."""
+    ok16 = ctypes.c_void_p(4096)
+    for kind, T in ((B.SV_PROBS, 1.0), (B.SV_LOGITS, 0.0)):
+        d = B.accept_desc(4, 8, 1024, kind, B.SV_F32, T)
+        st = lib.sv_spec_accept_stats(ctypes.byref(d), ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, None,
+                                      ok16, 1 << 20, None)
+        assert st == B.SV_ERR_INVALID_ARG and "rejection sampling" in B.last_error()
+    d = B.accept_desc(4, 8, 1024, B.SV_LOGITS, B.SV_F32)
+    need = lib.sv_spec_accept_workspace_size(ctypes.byref(d))
+    st = lib.sv_spec_accept_stats(ctypes.byref(d), ok16, ok16, None, ok16, ok16, ok16, ok16, ok16, ok16, None, ok16,
+                                  need, None)
+    assert st == B.SV_ERR_INVALID_ARG and "draft_stats" in B.last_error()
+    st = lib.sv_spec_accept_stats(ctypes.byref(d), ok16, ok16, ctypes.c_void_p(4096 + 4), ok16, ok16, ok16, ok16,
+                                  ok16, ok16, None, ok16, need, None)
+    assert st == B.SV_ERR_INVALID_ARG and "aligned" in B.last_error()
+    monkeypatch.setenv("SV_FAULT_INJECT", "launch")
+    st = lib.sv_spec_accept_stats(ctypes.byref(d), ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, None, ok16,
+                                  need, None)
+    assert st == B.SV_ERR_HIP and "sv_spec_accept_stats" in B.last_error()
