@@ -367,6 +367,20 @@ def main():
     assert torch.equal(rnd.accept_len, ref_out[0]) and torch.equal(rnd.out_tokens, ref_out[1])
     xs_bytes = float(rnd.K) * cfg.V * e_sz
 
+    # the same round captured once as a HIP graph and replayed: the launch shapes do not
+    # depend on the budget's choice, so one graph serves every round of this shape
+    gs = torch.cuda.Stream()
+    gs.wait_stream(stream)
+    with torch.cuda.stream(gs):
+        rnd.run()
+    stream.wait_stream(gs)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        rnd.run()
+    torch.cuda.synchronize()
+    t_graph = time_loop(torch, stream, graph.replay, args.steps)
+
     if args.copy_probe:
         log("copy probe")
         copy_probe()
@@ -412,7 +426,8 @@ def main():
                     "draft_stats_algorithmic_bytes": ds_bytes,
                     "acceptance_with_draft_stats_us": t_acc_stats * 1e3,
                     "acceptance_with_draft_stats_gbs": xs_bytes / (t_acc_stats * 1e-3) / 1e9,
-                    "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes},
+                    "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes,
+                    "graph_step_us": t_graph * 1e3},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
         "cpu_baseline": cpu,
     }
