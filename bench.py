@@ -160,6 +160,33 @@ def copy_probe():
     del src, dst
 
 
+READ_PROBE_BYTES = 2 << 30  # streaming-read probe: 2 GiB, eight times the last-level cache
+
+
+def read_probe(steps=10):
+    """Measured streaming-read bandwidth (GB/s) of a plain kernel (libsvprobe.so: one
+    workgroup per 32 KB chunk, non-temporal 16-byte loads), the practical ceiling for
+    the HBM-bound kernels; mean of `steps` back-to-back reads of READ_PROBE_BYTES."""
+    import ctypes
+    import torch
+    from paper_2607_25852_amd import build
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.svprobe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    lib.svprobe_stream_read.restype = ctypes.c_int32
+    buf = torch.empty(READ_PROBE_BYTES // 4, dtype=torch.float32, device="cuda").uniform_()
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def once():
+        st = lib.svprobe_stream_read(buf.data_ptr(), READ_PROBE_BYTES, sink.data_ptr(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"svprobe_stream_read failed: {st}")
+
+    ms = time_loop(torch, stream, once, steps)
+    del buf
+    return READ_PROBE_BYTES / (ms * 1e-3) / 1e9
+
+
 def attn_bytes(cfg, L, k):
     """Algorithmic HBM bytes of one verify-attention call: every visible K and V row
     read once per kv-head, plus q read and out written once."""
@@ -231,6 +258,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c64_b16")
     ap.add_argument("--kv-split", type=int, default=0)
+    ap.add_argument("--rotate", type=int, default=3,
+                    help="copies of the round's inputs used in turn, so that every step reads from HBM rather "
+                         "than the 256 MB last-level cache")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="host time for the oracle baseline (0: skip)")
     ap.add_argument("--copy-probe", action="store_true", help="also run a 1 GiB copy kernel (counter calibration)")
     ap.add_argument("--summarize-trace", metavar="CSV", help="print a rocprofv3 kernel-stats CSV as markdown")
@@ -259,30 +289,34 @@ def main():
     cfg = synth.CONFIGS[args.workload]
     log("generating inputs", cfg.name)
     t0 = time.perf_counter()
-    rnd = DeviceRound(cfg, kind="logits", kv_split=args.kv_split)
+    rnds = [DeviceRound(cfg, kind="logits", kv_split=args.kv_split) for _ in range(max(1, args.rotate))]
+    rnd = rnds[0]
     torch.cuda.synchronize()
-    log(f"inputs resident ({time.perf_counter() - t0:.1f} s); K={rnd.K}")
+    log(f"inputs resident ({time.perf_counter() - t0:.1f} s, {len(rnds)} copies); K={rnd.K}")
     k = np.diff(rnd.qo_host)
     drafts = int(np.sum(k - 1))
 
     stream = torch.cuda.current_stream()
     for _ in range(args.warmup):
-        rnd.run()
+        for r in rnds:
+            r.run()
     torch.cuda.synchronize()
-    # the selection is deterministic: the timed steps see the same qo_indptr
-    assert np.array_equal(rnd.qo.cpu().numpy(), rnd.qo_host)
+    # the selection is deterministic: the timed steps see the same qo_indptr in every copy
+    for r in rnds:
+        assert np.array_equal(r.qo.cpu().numpy(), rnd.qo_host)
+    committed = int(np.sum(rnd.accept_len.cpu().numpy() + 1))
 
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for s in range(args.steps):
-        e = ev[s]
+        e, r = ev[s], rnds[s % len(rnds)]
         e[0].record(stream)
-        rnd.run_budget()
+        r.run_budget()
         e[1].record(stream)
-        rnd.run_attn()
+        r.run_attn()
         e[2].record(stream)
-        rnd.run_accept()
+        r.run_accept()
         e[3].record(stream)
     torch.cuda.synchronize()
     t_end = time.perf_counter()
@@ -381,6 +415,8 @@ def main():
     torch.cuda.synchronize()
     t_graph = time_loop(torch, stream, graph.replay, args.steps)
 
+    read_gbs = read_probe()
+    log(f"streaming-read probe: {read_gbs:.0f} GB/s")
     if args.copy_probe:
         log("copy probe")
         copy_probe()
@@ -413,7 +449,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (plan + split-KV attention + partial merge)",
                      "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "traffic_unit": "HBM bytes per call", "algorithmic_bytes": a_bytes,
-                     "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest()},
+                     "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest(),
+                     "measured_read_peak": read_gbs, "frac_of_measured_read_peak": a_gbs / read_gbs},
         "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
                     "acceptance_algorithmic_bytes": x_bytes,
@@ -429,6 +466,7 @@ def main():
                     "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes,
                     "graph_step_us": t_graph * 1e3},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
+        "committed_tokens_per_s": committed / (ms_step * 1e-3),
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)

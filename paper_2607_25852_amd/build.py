@@ -1,8 +1,10 @@
-"""Builds libspecverify.so (gfx950) in-tree with hipcc.
+"""Builds libspecverify.so and the measurement probe libsvprobe.so (gfx950) in-tree
+with hipcc.
 
 Every HIP source is compiled for gfx950 only, with packed-fp32 instruction
 selection disabled (-Xclang -target-feature -Xclang -packed-fp32-ops); the
-objects are linked into paper_2607_25852_amd/libspecverify.so next to this file.
+objects are linked into paper_2607_25852_amd/libspecverify.so (and libsvprobe.so)
+next to this file.
 """
 import os
 import subprocess
@@ -14,11 +16,13 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INC = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libspecverify.so")
+PROBE_LIB = os.path.join(HERE, "libsvprobe.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["sv_api.cpp", "budget.hip", "accept.hip", "attn.hip", "pack.hip"]
+PROBE_SOURCES = ["read_probe.hip"]
 COMMON = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-I" + INC, "-I" + CSRC,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
 
@@ -39,16 +43,21 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=4) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str, verbose: bool) -> None:
+    tmp = lib + ".tmp"
     cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    with ThreadPoolExecutor(max_workers=4) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES + PROBE_SOURCES))
+    _link(objs[:len(SOURCES)], LIB, verbose)
+    _link(objs[len(SOURCES):], PROBE_LIB, verbose)
     return LIB
 
 

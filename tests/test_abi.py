@@ -245,3 +245,22 @@ def test_accept_stats_checks(lib, monkeypatch):
     st = lib.sv_spec_accept_stats(ctypes.byref(d), ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, ok16, None, ok16,
                                   need, None)
     assert st == B.SV_ERR_HIP and "sv_spec_accept_stats" in B.last_error()
+
+
+def test_probe_header_declarations_are_exported():
+    """The measurement probe's header and library agree (libsvprobe.so, built with the
+    main library); an invalid call is refused on the host."""
+    from paper_2607_25852_amd import build
+    if not os.path.exists(build.PROBE_LIB):
+        build.build()
+    text = open(os.path.join(ROOT, "include", "svprobe.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = set(re.findall(r"\b(svprobe_[a-z_]+)\s*\(", text))
+    assert declared == {"svprobe_stream_read"}
+    lib = ctypes.CDLL(build.PROBE_LIB)
+    lib.svprobe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    lib.svprobe_stream_read.restype = ctypes.c_int32
+    assert lib.svprobe_stream_read(None, 32768, None, None) == -1
+    assert lib.svprobe_stream_read(ctypes.c_void_p(4096), 1000, ctypes.c_void_p(4096), None) == -1
+    assert lib.svprobe_stream_read(ctypes.c_void_p(4100), 32768, ctypes.c_void_p(4096), None) == -1
+
