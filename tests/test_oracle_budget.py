@@ -150,3 +150,16 @@ def test_invalid_arguments_are_rejected(orc):
         orc.budget(conf, "fixed", fixed_budget=1)  # below R
     with pytest.raises(ValueError):
         orc.budget(conf, "fixed", fixed_budget=7)  # above R*b
+
+
+def test_full_budget_keeps_everything(orc):
+    """FIXED mode with K = R*b (the tiny and c16_b16 workloads) selects every position:
+    n_i = D for all requests and qo_indptr = (0, b, 2b, ...)."""
+    from paper_2607_25852_amd import synth
+    for name in ("tiny", "c16_b16"):
+        cfg = synth.CONFIGS[name]
+        assert cfg.budget == ("fixed", cfg.R * cfg.b)
+        conf = synth.make_logits_round(cfg)["conf"]
+        res = orc.budget(conf, "fixed", fixed_budget=cfg.R * cfg.b)
+        assert (np.asarray(res["keep"]) == cfg.b - 1).all()
+        np.testing.assert_array_equal(res["qo_indptr"], np.arange(cfg.R + 1) * cfg.b)
