@@ -61,7 +61,7 @@ def recorded_traffic(workload):
 
 
 def short_name(name):
-    n = name.replace("void ", "").replace("sv::(anonymous namespace)::", "")
+    n = name.replace("void ", "").replace("sv::(anonymous namespace)::", "").replace("(anonymous namespace)::", "")
     depth = 0
     for i, ch in enumerate(n):
         if ch == "<":
@@ -221,10 +221,22 @@ def time_loop(torch, stream, fn, steps):
     return a.elapsed_time(b) / steps
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, rnd, min_seconds):
-    """The oracle, as it stands, on the same round: budget over the whole batch, then
-    attention (every row and head) and acceptance of every request; repeated until at
-    least min_seconds of host time have passed."""
+    """The oracle, as it stands, on the same round: the budget over the whole batch (as
+    the workload defines it), then attention (every row and head) and acceptance of every
+    request; repeated until at least min_seconds of host time have passed. Also the mean
+    host time of each part."""
     import numpy as np
     import oracle
     from paper_2607_25852_amd import synth
@@ -233,22 +245,35 @@ def cpu_baseline(cfg, rnd, min_seconds):
     kv = rnd.kv
     q = synth.pack_rows(kv["q_full"], qo)
     target = synth.pack_rows(rnd.lr["target_full"], qo)
-    cost = synth.profiled_cost(cfg.R, cfg.b)
+    mode = cfg.budget[0]
+    cost = synth.profiled_cost(cfg.R, cfg.b) if mode == "cost" else None
+    parts = dict(budget=0.0, attention=0.0, acceptance=0.0)
     reps = 0
     t0 = time.perf_counter()
     while True:
-        oracle.budget(rnd.lr["conf"], "cost", cost=cost)
+        ta = time.perf_counter()
+        if mode == "cost":
+            oracle.budget(rnd.lr["conf"], "cost", cost=cost)
+        elif mode == "fixed":
+            oracle.budget(rnd.lr["conf"], "fixed", fixed_budget=cfg.budget[1])
+        tb = time.perf_counter()
         oracle.attention(q, kv["k_cache"], kv["v_cache"], kv["page_table"], qo, rnd.kv_lens_host, dtype=cfg.dtype)
+        tc = time.perf_counter()
         oracle.accept(target, rnd.lr["draft"], rnd.lr["draft_tokens"], qo, rnd.ua_host, rnd.us_host,
                       kind="logits", dtype=cfg.dtype)
+        td = time.perf_counter()
+        parts["budget"] += tb - ta
+        parts["attention"] += tc - tb
+        parts["acceptance"] += td - tc
         reps += 1
-        dt = time.perf_counter() - t0
+        dt = td - t0
         if dt >= min_seconds:
             break
     drafts = float(np.sum(k - 1)) * reps
     return dict(value=drafts / dt, unit="verified draft tokens/s", cores=oracle.num_threads(), kind="oracle",
                 sample=f"the whole round ({cfg.R} requests, {int(np.sum(k - 1))} kept drafts: budget, attention "
-                       f"of every row and head, acceptance) repeated {reps}x in {dt:.1f} s")
+                       f"of every row and head, acceptance) repeated {reps}x in {dt:.1f} s",
+                cpu_model=cpu_model(), part_seconds={kk: v / reps for kk, v in parts.items()})
 
 
 def main():
