@@ -28,6 +28,7 @@ constexpr int kThreads = 256;
 constexpr int kStatsLoads = 4;  // 16-byte loads in flight per thread in rowstats (16 KB chunks)
 constexpr int kResChunk = 8192;  // vocabulary chunk of the residual sums
 constexpr int kResPer = kResChunk / kThreads;  // tokens per thread in a chunk
+constexpr size_t kTsumMaxBytes = size_t(64) << 20;  // cap of the per-thread partial sums
 
 struct ReqPlan {
     int a, n, mode, flag;  // mode 0: residual after a rejection, 1: bonus, 2: nothing to draw
@@ -50,6 +51,7 @@ struct AcceptArgs {
     float2* stats_q;  // [R*D][NC]
     ReqPlan* plan;    // [R]
     uint64_t* csum;   // [R][NCR][2]
+    uint64_t* tsum;   // [R][NCR][kThreads] per-thread partial sums of column 0, or NULL
     int R, b, D, V, NC, stats_chunk, NCR, res_chunk;
     float invT;
 };
@@ -418,6 +420,7 @@ __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     } else {
         part = range_sum<LOGITS, T>(a, pl, 0, lo, hi);
     }
+    if (a.tsum) a.tsum[((size_t)i * a.NCR + c) * kThreads + tid] = part;
     const uint64_t sr = block_sum_u64(part, red);
     if (tid == 0) a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
 }
@@ -498,7 +501,46 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
         }
         __syncthreads();
         const int cs = s_chunk;
-        if (cs >= 0) {
+        if (cs >= 0 && col == 0 && a.tsum) {
+            // 2. inside the chunk, from the chunk-sum pass's per-thread partial sums: wave 0
+            //    finds the thread range holding thr (its 256 partials, 64 at a time), then
+            //    the token among that range's kResPer tokens, one weight per lane
+            if (w == 0) {
+                const uint64_t rel = thr - s_before;
+                const uint64_t* ts = a.tsum + ((size_t)i * a.NCR + cs) * kThreads;
+                uint64_t v4[kThreads / 64];
+#pragma unroll
+                for (int k = 0; k < kThreads / 64; k++) v4[k] = ts[k * 64 + lane];
+                uint64_t base = 0, before = 0;
+                int found = -1;
+#pragma unroll
+                for (int k = 0; k < kThreads / 64; k++) {
+                    if (found >= 0) break;
+                    const uint64_t incl = base + wave_incl_scan_u64(v4[k], lane);
+                    const uint64_t m = __ballot(v4[k] > 0 && incl - v4[k] <= rel && rel < incl);
+                    if (m) {
+                        const int src = __builtin_ctzll(m);
+                        found = k * 64 + src;
+                        before = __shfl(incl - v4[k], src, 64);
+                    }
+                    base = __shfl(incl, 63, 64);
+                }
+                int tok = -1;
+                if (found >= 0) {
+                    static_assert(kResPer <= 64, "one token per lane");
+                    const int beg = cs * kResChunk, end = min(a.V, beg + kResChunk);
+                    const int lo = min(end, beg + found * kResPer), hi = min(end, lo + kResPer);
+                    const int v = lo + lane;
+                    const uint64_t wv = lane < kResPer && v < hi ? weight_at<LOGITS, T>(a, pl, 0, v) : 0;
+                    const uint64_t incl = before + wave_incl_scan_u64(wv, lane);
+                    const uint64_t m = __ballot(wv > 0 && incl - wv <= rel && rel < incl);
+                    if (m) tok = lo + __builtin_ctzll(m);
+                }
+                if (lane == 0) s_token = tok;
+            }
+            __syncthreads();
+            token = s_token;
+        } else if (cs >= 0) {
             // 2. inside the chunk: per-thread contiguous ranges, block exclusive scan
             const int beg = cs * kResChunk, end = min(a.V, beg + kResChunk);
             const int lo = min(end, beg + tid * per), hi = min(end, lo + per);
@@ -744,6 +786,9 @@ AcceptPlan plan_accept(const sv_accept_desc& d) {
     off = al(off + R * sizeof(ReqPlan));
     p.off_csum = off;
     off = al(off + R * p.res_chunks * 2 * sizeof(uint64_t));
+    const size_t tsum_bytes = R * p.res_chunks * kThreads * sizeof(uint64_t);
+    p.off_tsum = tsum_bytes <= kTsumMaxBytes ? off : 0;
+    if (p.off_tsum) off = al(off + tsum_bytes);
     p.total = off;
     return p;
 }
@@ -769,6 +814,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     a.stats_q = (float2*)(w + p.off_stats_q);
     a.plan = (ReqPlan*)(w + p.off_plan);
     a.csum = (uint64_t*)(w + p.off_csum);
+    a.tsum = p.off_tsum ? (uint64_t*)(w + p.off_tsum) : nullptr;
     a.R = d.num_reqs;
     a.b = d.block;
     a.D = d.block - 1;
