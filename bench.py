@@ -299,8 +299,8 @@ def main():
         print(summarize_traffic(*args.summarize_traffic))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: the round's kernels run on a single MI355X and this build "
-              "has no multi-GPU path (see the sharding note in DESIGN.md); run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the round's kernels run on a single MI355X and the library "
+              "has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
