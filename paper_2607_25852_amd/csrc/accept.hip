@@ -71,13 +71,14 @@ __device__ inline V stream_load(const V* p) {
     return __builtin_nontemporal_load(p);
 }
 
-// fp32 probability of token v of a row: softmax(l / T) from its (max, 1/sum) in logits
-// mode, the stored value in probability mode. Every kernel uses this one function.
+// fp32 probability of token v of a row: softmax(l / T) from its (max m, 1/sum) in logits
+// mode, 2^(l * (log2e / T) - m * log2e) * (1/sum) with one fused multiply-add before the
+// exponent; the stored value in probability mode. The draw's weights (weight_xy) compute
+// the same expression.
 template <bool LOGITS, typename T>
 __device__ inline float prob_of(const T* row, int v, float m, float iS, float invT) {
     if (LOGITS) {
-        const float x = load_x<T>(row, v) * invT;
-        return __builtin_amdgcn_exp2f((x - m) * kLog2e) * iS;
+        return __builtin_amdgcn_exp2f(__builtin_fmaf(load_x<T>(row, v), invT * kLog2e, -m * kLog2e)) * iS;
     } else {
         return load_x<T>(row, v);
     }
@@ -309,9 +310,11 @@ __device__ inline uint64_t weight_at(const AcceptArgs& a, const ReqPlan& pl, int
 // the residual (or bonus) weight, column 1 the fallback weight of P_a
 template <bool LOGITS>
 __device__ inline uint64_t weight_xy(const ReqPlan& pl, int col, float x, float y, float invT) {
-    const float pv = LOGITS ? __builtin_amdgcn_exp2f((x * invT - pl.mP) * kLog2e) * pl.iSP : x;
+    // the probability of prob_of, with the row's constants hoisted out of the token loop
+    const float c = invT * kLog2e;
+    const float pv = LOGITS ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, c, -pl.mP * kLog2e)) * pl.iSP : x;
     if (pl.mode != 0 || col == 1) return weight_of(pv);
-    const float qv = LOGITS ? __builtin_amdgcn_exp2f((y * invT - pl.mQ) * kLog2e) * pl.iSQ : y;
+    const float qv = LOGITS ? __builtin_amdgcn_exp2f(__builtin_fmaf(y, c, -pl.mQ * kLog2e)) * pl.iSQ : y;
     float r = pv - qv;
     if (!(r > 0.0f)) r = 0.0f;
     return weight_of(r);
