@@ -30,6 +30,13 @@ ATTN_SRC = os.path.join(ROOT, "paper_2607_25852_amd", "csrc", "attn.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sv_verify_attn_c64_b16_traffic.md")
 COPY_BYTES = 1 << 30  # copy-probe size: 1 GiB read + 1 GiB written, well above the 256 MB MALL
 ATTN_KERNELS = ("attn_plan_kernel", "attn_bf16_kernel", "attn_merge_kernel")
+ACCEPT_KERNELS = ("rowstats_kernel", "decide_kernel", "chunksum_kernel", "search_kernel")
+# per call kind: its kernels, the kernel dispatched once per call, where the bench records
+# the call's algorithmic bytes
+TRAFFIC_CALLS = {
+    "attention": (ATTN_KERNELS, "attn_bf16_kernel", ("roofline", "algorithmic_bytes")),
+    "acceptance": (ACCEPT_KERNELS, "rowstats_kernel", ("kernels", "acceptance_algorithmic_bytes")),
+}
 
 
 def log(*a):
@@ -92,8 +99,10 @@ def summarize_trace(stats_csv):
     return "\n".join(out)
 
 
-def summarize_traffic(fetch_dir, write_dir):
-    """FETCH_SIZE / WRITE_SIZE per dispatch, scaled by the copy probe, as traffic per call."""
+def summarize_traffic(fetch_dir, write_dir, call="attention"):
+    """FETCH_SIZE / WRITE_SIZE per dispatch, scaled by the copy probe, as traffic per call
+    of `call` (attention: sv_verify_attn; acceptance: sv_spec_accept)."""
+    kernels, main_kernel, alg_key = TRAFFIC_CALLS[call]
     import csv
     import collections
 
@@ -118,13 +127,13 @@ def summarize_traffic(fetch_dir, write_dir):
     f_write = COPY_BYTES / (copy_write_kib * 1024)
     out = ["| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |", "|---|---|---|---|"]
     for k in sorted(set(fetch) | set(write)):
-        if not (any(a in k for a in ATTN_KERNELS) or "neg_kernel" in k):
+        if not (any(a in k for a in kernels) or "neg_kernel" in k):
             continue
         fv, wv = fetch.get(k, [0.0]), write.get(k, [0.0])
         out.append(f"| `{short_name(k)}` | {len(fv)} | {sum(fv) / len(fv):.0f} | {sum(wv) / len(wv):.0f} |")
-    main_calls = sum(len(v) for k, v in fetch.items() if "attn_bf16_kernel" in k)
-    tf = sum(sum(v) for k, v in fetch.items() if any(a in k for a in ATTN_KERNELS)) / main_calls
-    tw = sum(sum(v) for k, v in write.items() if any(a in k for a in ATTN_KERNELS)) / main_calls
+    main_calls = sum(len(v) for k, v in fetch.items() if main_kernel in k)
+    tf = sum(sum(v) for k, v in fetch.items() if any(a in k for a in kernels)) / main_calls
+    tw = sum(sum(v) for k, v in write.items() if any(a in k for a in kernels)) / main_calls
     traffic = tf * 1024 * f_fetch + tw * 1024 * f_write
     bench = {}
     bj = os.path.join(fetch_dir, "bench.json")
@@ -132,7 +141,7 @@ def summarize_traffic(fetch_dir, write_dir):
         lines = [l for l in open(bj) if l.startswith("{")]
         if lines:
             bench = json.loads(lines[-1])
-    alg = bench.get("roofline", {}).get("algorithmic_bytes")
+    alg = bench.get(alg_key[0], {}).get(alg_key[1])
     out += ["",
             f"- copy probe: {COPY_BYTES} bytes read and written; FETCH_SIZE {copy_fetch_kib:.0f} KiB, "
             f"WRITE_SIZE {copy_write_kib:.0f} KiB; scale factors fetch {f_fetch:.4f}, write {f_write:.4f}",
@@ -143,8 +152,8 @@ def summarize_traffic(fetch_dir, write_dir):
     if alg:
         out.append(f"- algorithmic_bytes_per_call: {alg:.0f} (traffic / algorithmic = {traffic / alg:.3f})")
     out.append(f"- workload: {bench.get('config', {}).get('workload', '?').split(':')[0]}")
-    # the digest of the source that ran (recorded by the bench run itself)
-    out.append(f"- attn_source_sha256: {bench.get('roofline', {}).get('attn_source_sha256', '?')}")
+    if call == "attention":  # the digest of the source that ran (recorded by the bench run itself)
+        out.append(f"- attn_source_sha256: {bench.get('roofline', {}).get('attn_source_sha256', '?')}")
     return "\n".join(out)
 
 
@@ -225,6 +234,21 @@ def time_loop(torch, stream, fn, steps):
     return a.elapsed_time(b) / steps
 
 
+def workload_text(cfg):
+    """One-line description of a workload from its configuration."""
+    kind = cfg.kv[0]
+    if kind == "lognormal":
+        ctx = f"lognormal context median {cfg.kv[1]} in [{cfg.kv[3]}, {cfg.kv[4]}]"
+    elif kind == "uniform":
+        ctx = f"context uniform in [{cfg.kv[1]}, {cfg.kv[2]}]"
+    else:
+        ctx = "contexts " + "/".join(str(x) for x in cfg.kv[1:])
+    budget = {"cost": "cost-table budget", "given": "verify depths k_i ~ U{1..b} given"}.get(
+        cfg.budget[0], f"fixed budget K={cfg.budget[1] if len(cfg.budget) > 1 else '?'}")
+    return (f"{cfg.name}: concurrency {cfg.R}, block {cfg.b}, Hq {cfg.Hq}/Hkv {cfg.Hkv}/d {cfg.d}, {ctx}, "
+            f"page {cfg.page}, vocab {cfg.V}, {budget}")
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -294,13 +318,18 @@ def main():
     ap.add_argument("--copy-probe", action="store_true", help="also run a 1 GiB copy kernel (counter calibration)")
     ap.add_argument("--summarize-trace", metavar="CSV", help="print a rocprofv3 kernel-stats CSV as markdown")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
-                    help="print HBM traffic per sv_verify_attn call from two rocprofv3 --pmc runs")
+                    help="print HBM traffic per call from two rocprofv3 --pmc runs")
+    ap.add_argument("--traffic-call", choices=sorted(TRAFFIC_CALLS), default="attention",
+                    help="the call --summarize-traffic reports")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the steps only: no greedy, packing, draft-statistics, graph or read-probe figures "
+                         "(for counter runs)")
     args = ap.parse_args()
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
         return
     if args.summarize_traffic:
-        print(summarize_traffic(*args.summarize_traffic))
+        print(summarize_traffic(*args.summarize_traffic, call=args.traffic_call))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the round's kernels run on a single MI355X and the library "
@@ -361,91 +390,108 @@ def main():
     log(f"step {ms_step:.3f} ms: budget {t_budget * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us "
         f"({a_gbs:.0f} GB/s), acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
 
-    # greedy verification (temperature 0) on the same round, outside the timed steps: the
-    # argmax pass reads only the kept target rows
-    gdesc = binding.accept_desc(cfg.R, cfg.b, cfg.V, binding.SV_LOGITS,
-                                binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16, 0.0)
-    gws = torch.empty(max(binding.accept_workspace_size(gdesc), 256), dtype=torch.uint8, device="cuda")
+    def post_step_figures():
+        """Figures of the calls outside the step, on the same round (first input copy)."""
+        # greedy verification (temperature 0) on the same round, outside the timed steps: the
+        # argmax pass reads only the kept target rows
+        gdesc = binding.accept_desc(cfg.R, cfg.b, cfg.V, binding.SV_LOGITS,
+                                    binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16, 0.0)
+        gws = torch.empty(max(binding.accept_workspace_size(gdesc), 256), dtype=torch.uint8, device="cuda")
 
-    def greedy():
-        binding.spec_accept(gdesc, rnd.target, None, rnd.tokens, rnd.qo, None, None, rnd.accept_len,
-                            rnd.out_tokens, rnd.flags, gws)
+        def greedy():
+            binding.spec_accept(gdesc, rnd.target, None, rnd.tokens, rnd.qo, None, None, rnd.accept_len,
+                                rnd.out_tokens, rnd.flags, gws)
 
-    t_greedy = time_loop(torch, stream, greedy, args.steps)
-    g_bytes = float(rnd.K) * cfg.V * (4 if cfg.dtype == "f32" else 2)
+        t_greedy = time_loop(torch, stream, greedy, args.steps)
+        g_bytes = float(rnd.K) * cfg.V * (4 if cfg.dtype == "f32" else 2)
 
-    # packing of the verify batch and the KV append of the same round, outside the timed
-    # steps; the append writes the kept positions' own keys and values (gathered from the
-    # cache) back to their slots, so the round's cache is unchanged
-    e_sz = 4 if cfg.dtype == "f32" else 2
-    pt_h = rnd.kv["page_table"]
-    k_new_h = np.empty((rnd.K, cfg.Hkv, cfg.d), rnd.kv["k_cache"].dtype)
-    v_new_h = np.empty_like(k_new_h)
-    for i in range(cfg.R):
-        for j in range(int(k[i])):
-            s_ = int(rnd.L[i]) + j
-            k_new_h[rnd.qo_host[i] + j] = rnd.kv["k_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
-            v_new_h[rnd.qo_host[i] + j] = rnd.kv["v_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
-    k_new, v_new = to_dev(k_new_h), to_dev(v_new_h)
-    ctx = to_dev(np.asarray(rnd.L, np.int32))
-    blk_tok = to_dev(np.random.default_rng(cfg.seed).integers(0, cfg.V, size=(cfg.R, cfg.b)).astype(np.int32))
-    p_tok = torch.empty(cfg.R * cfg.b, dtype=torch.int32, device="cuda")
-    p_pos = torch.empty_like(p_tok)
-    p_kvl = torch.empty(cfg.R, dtype=torch.int32, device="cuda")
-    pdesc = binding.pack_desc(cfg.R, cfg.b, cfg.R * cfg.b)
-    apdesc = binding.append_desc(cfg.R, rnd.K, cfg.b, cfg.Hkv, cfg.d, cfg.page, pt_h.shape[1], rnd.kv["num_pages"],
-                                 binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
+        # packing of the verify batch and the KV append of the same round, outside the timed
+        # steps; the append writes the kept positions' own keys and values (gathered from the
+        # cache) back to their slots, so the round's cache is unchanged
+        e_sz = 4 if cfg.dtype == "f32" else 2
+        pt_h = rnd.kv["page_table"]
+        k_new_h = np.empty((rnd.K, cfg.Hkv, cfg.d), rnd.kv["k_cache"].dtype)
+        v_new_h = np.empty_like(k_new_h)
+        for i in range(cfg.R):
+            for j in range(int(k[i])):
+                s_ = int(rnd.L[i]) + j
+                k_new_h[rnd.qo_host[i] + j] = rnd.kv["k_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
+                v_new_h[rnd.qo_host[i] + j] = rnd.kv["v_cache"][pt_h[i, s_ // cfg.page], :, s_ % cfg.page]
+        k_new, v_new = to_dev(k_new_h), to_dev(v_new_h)
+        ctx = to_dev(np.asarray(rnd.L, np.int32))
+        blk_tok = to_dev(np.random.default_rng(cfg.seed).integers(0, cfg.V, size=(cfg.R, cfg.b)).astype(np.int32))
+        p_tok = torch.empty(cfg.R * cfg.b, dtype=torch.int32, device="cuda")
+        p_pos = torch.empty_like(p_tok)
+        p_kvl = torch.empty(cfg.R, dtype=torch.int32, device="cuda")
+        pdesc = binding.pack_desc(cfg.R, cfg.b, cfg.R * cfg.b)
+        apdesc = binding.append_desc(cfg.R, rnd.K, cfg.b, cfg.Hkv, cfg.d, cfg.page, pt_h.shape[1], rnd.kv["num_pages"],
+                                     binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
 
-    def pack():
-        binding.pack_verify(pdesc, blk_tok, ctx, rnd.qo, p_tok, p_pos, p_kvl)
+        def pack():
+            binding.pack_verify(pdesc, blk_tok, ctx, rnd.qo, p_tok, p_pos, p_kvl)
 
-    def append():
-        binding.append_kv(apdesc, k_new, v_new, rnd.page_table, rnd.qo, ctx, rnd.k_cache, rnd.v_cache)
+        def append():
+            binding.append_kv(apdesc, k_new, v_new, rnd.page_table, rnd.qo, ctx, rnd.k_cache, rnd.v_cache)
 
-    t_pack = time_loop(torch, stream, pack, args.steps)
-    t_append = time_loop(torch, stream, append, args.steps)
-    assert np.array_equal(p_kvl.cpu().numpy(), rnd.kv_lens_host)
-    ap_bytes = 4.0 * rnd.K * cfg.Hkv * cfg.d * e_sz
+        t_pack = time_loop(torch, stream, pack, args.steps)
+        t_append = time_loop(torch, stream, append, args.steps)
+        assert np.array_equal(p_kvl.cpu().numpy(), rnd.kv_lens_host)
+        ap_bytes = 4.0 * rnd.K * cfg.Hkv * cfg.d * e_sz
 
-    # the drafter's side: softmax statistics and confidences of every draft row, then the
-    # acceptance that takes the draft rows' statistics instead of re-reading them (same
-    # outputs bit for bit), both on the same round and outside the timed steps
-    dsdesc = binding.draft_stats_desc(cfg.R, cfg.b - 1, cfg.V, binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
-    ds_ws = torch.empty(max(binding.draft_stats_workspace_size(dsdesc), 256), dtype=torch.uint8, device="cuda")
-    ds_stats = torch.empty((cfg.R * (cfg.b - 1), 2), dtype=torch.float32, device="cuda")
-    ds_conf = torch.empty(cfg.R * (cfg.b - 1), dtype=torch.float32, device="cuda")
+        # the drafter's side: softmax statistics and confidences of every draft row, then the
+        # acceptance that takes the draft rows' statistics instead of re-reading them (same
+        # outputs bit for bit), both on the same round and outside the timed steps
+        dsdesc = binding.draft_stats_desc(cfg.R, cfg.b - 1, cfg.V, binding.SV_F32 if cfg.dtype == "f32" else binding.SV_BF16)
+        ds_ws = torch.empty(max(binding.draft_stats_workspace_size(dsdesc), 256), dtype=torch.uint8, device="cuda")
+        ds_stats = torch.empty((cfg.R * (cfg.b - 1), 2), dtype=torch.float32, device="cuda")
+        ds_conf = torch.empty(cfg.R * (cfg.b - 1), dtype=torch.float32, device="cuda")
 
-    def dstats():
-        binding.draft_stats(dsdesc, rnd.draft, ds_stats, ds_conf, ds_ws)
+        def dstats():
+            binding.draft_stats(dsdesc, rnd.draft, ds_stats, ds_conf, ds_ws)
 
-    def accept_with_stats():
-        binding.spec_accept_stats(rnd.xdesc, rnd.target, rnd.draft, ds_stats, rnd.tokens, rnd.qo, rnd.u_accept,
-                                  rnd.u_sample, rnd.accept_len, rnd.out_tokens, rnd.flags, rnd.acc_ws)
+        def accept_with_stats():
+            binding.spec_accept_stats(rnd.xdesc, rnd.target, rnd.draft, ds_stats, rnd.tokens, rnd.qo, rnd.u_accept,
+                                      rnd.u_sample, rnd.accept_len, rnd.out_tokens, rnd.flags, rnd.acc_ws)
 
-    t_dstats = time_loop(torch, stream, dstats, args.steps)
-    ds_bytes = float(cfg.R * (cfg.b - 1)) * cfg.V * e_sz
-    rnd.run_accept()
-    ref_out = (rnd.accept_len.clone(), rnd.out_tokens.clone())
-    t_acc_stats = time_loop(torch, stream, accept_with_stats, args.steps)
-    assert torch.equal(rnd.accept_len, ref_out[0]) and torch.equal(rnd.out_tokens, ref_out[1])
-    xs_bytes = float(rnd.K) * cfg.V * e_sz
+        t_dstats = time_loop(torch, stream, dstats, args.steps)
+        ds_bytes = float(cfg.R * (cfg.b - 1)) * cfg.V * e_sz
+        rnd.run_accept()
+        ref_out = (rnd.accept_len.clone(), rnd.out_tokens.clone())
+        t_acc_stats = time_loop(torch, stream, accept_with_stats, args.steps)
+        assert torch.equal(rnd.accept_len, ref_out[0]) and torch.equal(rnd.out_tokens, ref_out[1])
+        xs_bytes = float(rnd.K) * cfg.V * e_sz
 
-    # the same round captured once as a HIP graph and replayed: the launch shapes do not
-    # depend on the budget's choice, so one graph serves every round of this shape
-    gs = torch.cuda.Stream()
-    gs.wait_stream(stream)
-    with torch.cuda.stream(gs):
-        rnd.run()
-    stream.wait_stream(gs)
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        rnd.run()
-    torch.cuda.synchronize()
-    t_graph = time_loop(torch, stream, graph.replay, args.steps)
+        # the same round captured once as a HIP graph and replayed: the launch shapes do not
+        # depend on the budget's choice, so one graph serves every round of this shape
+        gs = torch.cuda.Stream()
+        gs.wait_stream(stream)
+        with torch.cuda.stream(gs):
+            rnd.run()
+        stream.wait_stream(gs)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            rnd.run()
+        torch.cuda.synchronize()
+        t_graph = time_loop(torch, stream, graph.replay, args.steps)
 
-    read_gbs = read_probe()
-    log(f"streaming-read probe: {read_gbs:.0f} GB/s")
+        return {"greedy_acceptance_us": t_greedy * 1e3,
+                "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
+                "greedy_acceptance_algorithmic_bytes": g_bytes,
+                "pack_us": t_pack * 1e3, "append_us": t_append * 1e3,
+                "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes,
+                "draft_stats_us": t_dstats * 1e3, "draft_stats_gbs": ds_bytes / (t_dstats * 1e-3) / 1e9,
+                "draft_stats_algorithmic_bytes": ds_bytes,
+                "acceptance_with_draft_stats_us": t_acc_stats * 1e3,
+                "acceptance_with_draft_stats_gbs": xs_bytes / (t_acc_stats * 1e-3) / 1e9,
+                "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes,
+                "graph_step_us": t_graph * 1e3}
+
+    extra = {} if args.step_only else post_step_figures()
+    read_gbs = None
+    if not args.step_only:
+        read_gbs = read_probe()
+        log(f"streaming-read probe: {read_gbs:.0f} GB/s")
     if args.copy_probe:
         log("copy probe")
         copy_probe()
@@ -469,9 +515,7 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": f"{cfg.name}: concurrency {cfg.R}, block {cfg.b}, Hq {cfg.Hq}/Hkv {cfg.Hkv}/d {cfg.d}, "
-                               f"lognormal context median 4096 in [512, 32768], page {cfg.page}, vocab {cfg.V}, "
-                               f"cost-table budget",
+        "config": {"workload": workload_text(cfg),
                    "concurrency": cfg.R, "block": cfg.b, "verified_positions": int(rnd.K),
                    "verified_drafts": drafts, "budget_ratio_index": int(rnd.sel[1].item()),
                    "parallelism": "single GPU"},
@@ -479,21 +523,12 @@ def main():
                      "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "traffic_unit": "HBM bytes per call", "algorithmic_bytes": a_bytes,
                      "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest(),
-                     "measured_read_peak": read_gbs, "frac_of_measured_read_peak": a_gbs / read_gbs},
+                     "measured_read_peak": read_gbs,
+                     "frac_of_measured_read_peak": a_gbs / read_gbs if read_gbs else None},
         "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
                     "acceptance_algorithmic_bytes": x_bytes,
-                    "greedy_acceptance_us": t_greedy * 1e3,
-                    "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
-                    "greedy_acceptance_algorithmic_bytes": g_bytes,
-                    "pack_us": t_pack * 1e3, "append_us": t_append * 1e3,
-                    "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes,
-                    "draft_stats_us": t_dstats * 1e3, "draft_stats_gbs": ds_bytes / (t_dstats * 1e-3) / 1e9,
-                    "draft_stats_algorithmic_bytes": ds_bytes,
-                    "acceptance_with_draft_stats_us": t_acc_stats * 1e3,
-                    "acceptance_with_draft_stats_gbs": xs_bytes / (t_acc_stats * 1e-3) / 1e9,
-                    "acceptance_with_draft_stats_algorithmic_bytes": xs_bytes,
-                    "graph_step_us": t_graph * 1e3},
+                    **extra},
         "verified_positions_per_s": rnd.K / (ms_step * 1e-3),
         "committed_tokens_per_s": committed / (ms_step * 1e-3),
         "cpu_baseline": cpu,
