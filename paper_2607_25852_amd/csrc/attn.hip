@@ -123,7 +123,14 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     constexpr int DT = HD / 32;             // output d-tiles
     constexpr int PF = NBUF - 1;            // prefetch distance in tiles
 
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    // The thread id passes through an empty asm statement, so the per-lane values derived
+    // from it (LDS and DMA offsets) are recomputed per item instead of being hoisted out
+    // of the persistent item loop, where the invariants of both wave mappings would stay
+    // live together (252 VGPRs instead of about 220, leaving no room for the operand
+    // prefetch in compute_tile).
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, w = tid >> 6;
     const int q0 = a.qo[i];
     const int k_i = a.qo[i + 1] - q0;
     int kv_len = a.kv_lens[i];
@@ -237,65 +244,181 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
         if (rg * 32 >= M) return;
         const uint16_t* kt = lds.kv[buf][0];
         const uint16_t* vt = lds.kv[buf][1];
-        // S^T = K Q^T for each 32-token half this wave owns (unscaled). Two independent
-        // accumulation chains keep the matrix pipe busy while K fragments arrive: the two
-        // halves (whole-tile waves), or the even and odd k-steps of one half.
+        // S^T = K Q^T for each 32-token half this wave owns (unscaled), as two independent
+        // accumulation chains: the two halves (whole-tile waves), or the even and odd
+        // k-steps of one half. Each K fragment is read from LDS KPD MFMAs before the MFMA
+        // that consumes it; the scheduling barriers keep that order, so the LDS latency
+        // runs under the matrix pipe instead of stalling every MFMA.
         f32x16 sacc[NSB];
         {
             const int sw = swz(lane & 31) & (CPR - 1);  // swz depends on t % 16 only
             const uint16_t* krow0 = kt + ((HALVES == 2 ? th : 0) * 32 + (lane & 31)) * HD;
+            constexpr int NF = NSB * KK;  // K fragments (= MFMAs) per tile
+            constexpr int KPD = 4;
+            // fragment j: whole-tile waves alternate the token halves (j % 2) at k-step j / 2;
+            // half-tile waves take k-step j of their half
+            auto kaddr = [&](int j) {
+                if constexpr (NSB == 2) return krow0 + (j & 1) * 32 * HD + (((2 * (j >> 1) + half) ^ sw) << 3);
+                else return krow0 + (((2 * j + half) ^ sw) << 3);
+            };
+            bf16x8 kb[KPD + 1];
+            f32x16 c0 = f32x16{}, c1 = f32x16{};
+#pragma unroll
+            for (int j = 0; j < KPD; j++) kb[j] = __builtin_bit_cast(bf16x8, *(const u16x8*)kaddr(j));
+#pragma unroll
+            for (int j = 0; j < NF; j++) {
+                if (j + KPD < NF) kb[(j + KPD) % (KPD + 1)] = __builtin_bit_cast(bf16x8, *(const u16x8*)kaddr(j + KPD));
+                __builtin_amdgcn_sched_barrier(0);
+                const bf16x8 bq = NSB == 2 ? qf[j >> 1] : qf[j];
+                if (j & 1) c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[j % (KPD + 1)], bq, c1, 0, 0, 0);
+                else c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb[j % (KPD + 1)], bq, c0, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
             if constexpr (NSB == 2) {
-                sacc[0] = f32x16{};
-                sacc[1] = f32x16{};
-#pragma unroll
-                for (int kk = 0; kk < KK; kk++) {
-                    const int off = ((2 * kk + half) ^ sw) << 3;
-                    const bf16x8 a0 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + off));
-                    const bf16x8 a1 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + 32 * HD + off));
-                    sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kk], sacc[0], 0, 0, 0);
-                    sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kk], sacc[1], 0, 0, 0);
-                }
+                sacc[0] = c0;
+                sacc[1] = c1;
             } else {
-                f32x16 s0 = f32x16{}, s1 = f32x16{};
-#pragma unroll
-                for (int kk = 0; kk < KK; kk += 2) {
-                    const bf16x8 a0 = __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + (((2 * kk + half) ^ sw) << 3)));
-                    const bf16x8 a1 =
-                        __builtin_bit_cast(bf16x8, *(const u16x8*)(krow0 + (((2 * kk + 2 + half) ^ sw) << 3)));
-                    s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[kk], s0, 0, 0, 0);
-                    s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[kk + 1], s1, 0, 0, 0);
-                }
-                sacc[0] = s0 + s1;
+                sacc[0] = c0 + c1;
             }
         }
-        // Each owned half is one online-softmax step (its own max, lazy rescale, exponent
-        // and PV update), so the softmax of the first half overlaps the MFMAs of the second.
-        // Causal/tail mask on the raw scores: register e of half hh holds token
-        // tb + 32hh + 4*half + (8(e/4) + e%4), masked when that token is past the row's last
-        // visible key or the split end. Only halves reaching past L (the first row's limit)
-        // or the split end need it, a wave-uniform test. Padding rows (r >= M) are not
-        // masked: their query is zero, and their output column is neither written nor
-        // mixed into the other columns.
-        const int g = lane >> 4, jl = lane & 15;
-#pragma unroll
-        for (int sb = 0; sb < NSB; sb++) {
-            const int hh = HALVES == 2 ? th : sb;
+        if constexpr (NSB == 2) {
+            // Causal/tail mask on the raw scores: register e of half hh holds token
+            // tb + 32hh + 4*half + (8(e/4) + e%4), masked when that token is past the row's last
+            // visible key or the split end. Only halves reaching past L (the first row's limit)
+            // or the split end need it, a wave-uniform test. Padding rows (r >= M) are not
+            // masked: their query is zero, and their output column is neither written nor
+            // mixed into the other columns.
+    #pragma unroll
+            for (int sb = 0; sb < NSB; sb++) {
+                const int tb_h = tb + (HALVES == 2 ? th : sb) * 32;
+                if (tb_h + 31 > L || tb_h + 32 > tok_end) {
+                    const int dlim = last_key - tb_h - 4 * half;  // mask where 8(e/4) + e%4 > dlim
+    #pragma unroll
+                    for (int e = 0; e < 16; e++)
+                        if (8 * (e >> 2) + (e & 3) > dlim) sacc[sb][e] = -INFINITY;
+                }
+            }
+            // One online-softmax step per tile over the owned halves: the row max (lane-local,
+            // then across the lane halves: the row's other 16 scores sit in lane l ^ 32, and
+            // v_permlane32_swap with both operands = mx returns the lower half's values in one
+            // result and the upper half's in the other), then a lazy rescale: the running max
+            // moves only when a score exceeds it by more than 8 (log2 units), so p = 2^(z - m)
+            // <= 256 stays exact in fp32 and bf16, and most tiles skip the accumulator rescale.
+            float mx = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), sacc[0][2]);
+    #pragma unroll
+            for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[0][e]), sacc[0][e + 1]);
+            mx = fmaxf(mx, sacc[0][15]);
+            if constexpr (NSB == 2) {
+    #pragma unroll
+                for (int e = 0; e < 16; e += 2) mx = fmaxf(fmaxf(mx, sacc[1][e]), sacc[1][e + 1]);
+            }
+            {
+                const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+                mx = fmaxf(__uint_as_float(sw2[0]), __uint_as_float(sw2[1]));
+            }
+            const float mxs = mx * a.scale_log2;  // max in scaled log2 units (-inf: all masked)
+            if (__any(mxs > m_run + 8.0f)) {
+                const float m_new = fmaxf(m_run, mxs);
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+    #pragma unroll
+                for (int t = 0; t < DT; t++) o[t] *= alpha;
+                m_run = m_new;
+            }
+            const float nm = -m_run;
+
+            // O^T += V^T P^T. MFMA J of the tile: half J / NJ (whole-tile waves; else this
+            // wave's half), 16-token k-chunk (J % NJ) / DT of that half, d-tile J % DT. The V^T
+            // operand comes from two transpose reads: in 16-lane group g = lane/16, input lane
+            // jl addresses token 16c + 8q + 4(g/2) + jl/4 at dims 32t + 16(g%2) + 4(jl%4) .. +3,
+            // and output lane jl receives dim 32t + 16(g%2) + jl of tokens 16c + 8q + 4(g/2) +
+            // 0..3. The operands are read VPD MFMAs ahead; the first VPD are in flight while the
+            // exponents of the first half are computed.
+            const int g = lane >> 4, jl = lane & 15;
+            constexpr int NJ = 2 * DT;    // PV MFMAs per 32-token half
+            constexpr int NT = NSB * NJ;  // PV MFMAs per tile for this wave
+            constexpr int VPD = 4;
+            auto vread = [&](int J) {
+                const int hh = HALVES == 2 ? th : J / NJ;
+                const int c = 2 * hh + (J % NJ) / DT, t = J % DT;
+                i16x4 vq[2];
+    #pragma unroll
+                for (int qh = 0; qh < 2; qh++) {
+                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
+                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
+                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
+                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                    vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
+                }
+                return __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
+            };
+            i16x8 vb[VPD + 1];
+    #pragma unroll
+            for (int j = 0; j < VPD; j++) vb[j] = vread(j);
+            __builtin_amdgcn_sched_barrier(0);
+            // p = 2^(z * scale * log2e - m) of the first half, its row sum, and the bf16 P^T
+            // fragments (already in the B-operand layout)
+            float ps0 = 0.0f, ps1 = 0.0f;
+    #pragma unroll
+            for (int e = 0; e < 16; e++) {
+                sacc[0][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[0][e], a.scale_log2, nm));
+                ps0 += sacc[0][e];
+            }
+            bf16x8 pb[NSB][2];
+    #pragma unroll
+            for (int cc = 0; cc < 2; cc++)
+    #pragma unroll
+                for (int e = 0; e < 8; e++) pb[0][cc][e] = (__bf16)sacc[0][8 * cc + e];
+            __builtin_amdgcn_sched_barrier(0);
+            // PV MFMAs. Whole-tile waves compute the second half's exponents between the first
+            // half's MFMAs (16 / NJ per MFMA), so the vector ALU works under the matrix pipe.
+    #pragma unroll
+            for (int J = 0; J < NT; J++) {
+                if (J + VPD < NT) vb[(J + VPD) % (VPD + 1)] = vread(J + VPD);
+                __builtin_amdgcn_sched_barrier(0);
+                const int t = J % DT;
+                o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vb[J % (VPD + 1)]),
+                                                                pb[J / NJ][(J % NJ) / DT], o[t], 0, 0, 0);
+                if constexpr (NSB == 2) {
+                    if (J < NJ) {
+                        constexpr int EPM = 16 / NJ;
+    #pragma unroll
+                        for (int x = 0; x < EPM; x++) {
+                            const int e = EPM * J + x;
+                            sacc[1][e] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[1][e], a.scale_log2, nm));
+                            ps1 += sacc[1][e];
+                        }
+                        if (J == NJ - 1) {
+    #pragma unroll
+                            for (int cc = 0; cc < 2; cc++)
+    #pragma unroll
+                                for (int e = 0; e < 8; e++) pb[1][cc][e] = (__bf16)sacc[1][8 * cc + e];
+                        }
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            l_run += ps0 + ps1;
+        } else {
+            // Half-tile waves: one online-softmax step per tile on the wave's half.
+            const int g = lane >> 4, jl = lane & 15;
+            const int hh = th;
             const int tb_h = tb + hh * 32;
             if (tb_h + 31 > L || tb_h + 32 > tok_end) {
                 const int dlim = last_key - tb_h - 4 * half;  // mask where 8(e/4) + e%4 > dlim
 #pragma unroll
                 for (int e = 0; e < 16; e++)
-                    if (8 * (e >> 2) + (e & 3) > dlim) sacc[sb][e] = -INFINITY;
+                    if (8 * (e >> 2) + (e & 3) > dlim) sacc[0][e] = -INFINITY;
             }
-            float mx = fmaxf(fmaxf(sacc[sb][0], sacc[sb][1]), sacc[sb][2]);
+            float mx = fmaxf(fmaxf(sacc[0][0], sacc[0][1]), sacc[0][2]);
 #pragma unroll
-            for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[sb][e]), sacc[sb][e + 1]);
-            mx = fmaxf(mx, sacc[sb][15]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float mxs = mx * a.scale_log2;  // max in scaled log2 units (-inf: all masked)
-            // lazy rescale: the running max moves only when a score exceeds it by more than
-            // 8, so p = 2^(z - m) <= 256 stays exact in fp32 and bf16, and most steps skip
-            // the rescale of the accumulators
+            for (int e = 3; e < 15; e += 2) mx = fmaxf(fmaxf(mx, sacc[0][e]), sacc[0][e + 1]);
+            mx = fmaxf(mx, sacc[0][15]);
+            {
+                const auto sw2 = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+                mx = fmaxf(__uint_as_float(sw2[0]), __uint_as_float(sw2[1]));
+            }
+            const float mxs = mx * a.scale_log2;
             if (__any(mxs > m_run + 8.0f)) {
                 const float m_new = fmaxf(m_run, mxs);
                 const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -304,41 +427,48 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
                 for (int t = 0; t < DT; t++) o[t] *= alpha;
                 m_run = m_new;
             }
+            constexpr int NJ = 2 * DT;
+            constexpr int VPD = 4;
+            auto vread = [&](int j) {
+                const int c = 2 * hh + j / DT, t = j % DT;
+                i16x4 vq[2];
+#pragma unroll
+                for (int qh = 0; qh < 2; qh++) {
+                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
+                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
+                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
+                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                    vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
+                }
+                return __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
+            };
+            i16x8 vb[VPD + 1];
+#pragma unroll
+            for (int j = 0; j < VPD; j++) vb[j] = vread(j);
+            __builtin_amdgcn_sched_barrier(0);
             const float nm = -m_run;
             float psum = 0.0f;
 #pragma unroll
             for (int e = 0; e < 16; e++) {
-                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[sb][e], a.scale_log2, nm));
-                sacc[sb][e] = p;
+                const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[0][e], a.scale_log2, nm));
+                sacc[0][e] = p;
                 psum += p;
             }
             l_run += psum;
-
-            // O^T += V^T P^T over the two 16-token k-chunks of this half. The V^T operand
-            // comes from two transpose reads: in 16-lane group g = lane/16, input lane j
-            // addresses token 16c + 8q + 4(g/2) + j/4 at dims 32t + 16(g%2) + 4(j%4) .. +3,
-            // and output lane j receives dim 32t + 16(g%2) + j of tokens
-            // 16c + 8q + 4(g/2) + 0..3.
+            bf16x8 pb[2];
 #pragma unroll
-            for (int cc = 0; cc < 2; cc++) {
-                const int c = 2 * hh + cc;
-                bf16x8 pb;
+            for (int cc = 0; cc < 2; cc++)
 #pragma unroll
-                for (int e = 0; e < 8; e++) pb[e] = (__bf16)sacc[sb][8 * cc + e];
+                for (int e = 0; e < 8; e++) pb[cc][e] = (__bf16)sacc[0][8 * cc + e];
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int t = 0; t < DT; t++) {
-                    i16x4 vq[2];
-#pragma unroll
-                    for (int qh = 0; qh < 2; qh++) {
-                        const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
-                        const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
-                        const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
-                        const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
-                        vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
-                    }
-                    const i16x8 vv = __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
-                    o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vv), pb, o[t], 0, 0, 0);
-                }
+            for (int j = 0; j < NJ; j++) {
+                if (j + VPD < NJ) vb[(j + VPD) % (VPD + 1)] = vread(j + VPD);
+                __builtin_amdgcn_sched_barrier(0);
+                const int t = j % DT;
+                o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vb[j % (VPD + 1)]), pb[j / DT],
+                                                                o[t], 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     };
