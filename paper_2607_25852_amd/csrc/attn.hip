@@ -136,7 +136,8 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     int kv_len = a.kv_lens[i];
     if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
     const int L = kv_len - k_i;
-    if (k_i <= 0 || k_i > a.block || L < 0 || q0 < 0 || q0 + k_i > a.total_q) return;
+    // (bitwise or: both descriptor loads are issued before the test)
+    if ((k_i <= 0) | (k_i > a.block) | (L < 0) | (q0 < 0) | (q0 + k_i > a.total_q)) return;
     const int tok_begin = s * a.split;
     if (tok_begin >= kv_len) return;
     const int tok_end = min(kv_len, tok_begin + a.split);
@@ -145,15 +146,14 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     const int M = min(a.G * k_i - row0, RB);  // rows of this item
     if (M <= 0) return;
 
-    // page ids of this split -> LDS (the host keeps a split within 1024 pages)
+    // page ids of this split -> LDS (the host keeps a split within 1024 pages). The first
+    // page id of each thread is loaded before the query fragments and stored after them,
+    // so the two round trips overlap.
     const int slot0 = tok_begin >> a.log2P;
     const int nslots = ((tok_end - 1) >> a.log2P) - slot0 + 1;
     const int32_t* __restrict__ pt = a.page_table + (size_t)i * a.maxp;
-    for (int e = tid; e < nslots; e += NW * 64) {
-        const int slot = slot0 + e;
-        const int pg = slot < a.maxp ? pt[slot] : -1;
-        lds.pid[e] = (pg >= 0 && pg < a.num_pages) ? pg : -1;
-    }
+    int pg0 = -1;
+    if (tid < nslots && slot0 + tid < a.maxp) pg0 = pt[slot0 + tid];
 
     // this lane's query row (N index of the MFMA) and its half (K-slice selector)
     // row group; token half of each tile (HALVES == 2), else the whole tile
@@ -178,6 +178,12 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
             u16x8 v = row_ok ? *(const u16x8*)(src + kk * 16 + half * 8) : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
             qf[kk] = __builtin_bit_cast(bf16x8, v);
         }
+    }
+    if (tid < nslots) lds.pid[tid] = (pg0 >= 0 && pg0 < a.num_pages) ? pg0 : -1;
+    for (int e = tid + NW * 64; e < nslots; e += NW * 64) {
+        const int slot = slot0 + e;
+        const int pg = slot < a.maxp ? pt[slot] : -1;
+        lds.pid[e] = (pg >= 0 && pg < a.num_pages) ? pg : -1;
     }
     // the query fragments must have landed before the DMA ring starts: a wait the
     // compiler sees (vmcnt(0)) keeps it from re-checking them inside the loop, where
