@@ -841,12 +841,15 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     }
     int split = d.kv_split;
     if (split <= 0) {
-        // about 16 splits for the longest request, 4096..8192 tokens each: enough work
-        // items for the persistent grid to balance (largest first), while the partial
-        // results (written, then merged) stay a few percent of the KV bytes
-        long long want = ((long long)d.max_kv_len + 15) / 16;
+        // About 8 work items per compute unit if every request had the longest context:
+        // R * Hkv * max_kv_len head-tokens over 256 CUs, divided by 8, at least 4096
+        // tokens. Measured over split sizes 2048..24576, this picks the best or nearly the
+        // best one on c64_b16 (8192), long_c32 (8192) and the C5 c64 sweep (16384): fewer,
+        // longer items save per-item prologues and merge work until the last items to
+        // finish start to dominate. The host does not see the lengths themselves (they
+        // live on the device), so the bound uses max_kv_len.
+        long long want = (long long)d.num_reqs * d.num_kv_heads * d.max_kv_len / (256 * 8);
         if (want < 4096) want = 4096;
-        if (want > 8192) want = 8192;
         split = (int)(((want + 63) / 64) * 64);
     }
     if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
