@@ -842,14 +842,16 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     int split = d.kv_split;
     if (split <= 0) {
         // About 8 work items per compute unit if every request had the longest context:
-        // R * Hkv * max_kv_len head-tokens over 256 CUs, divided by 8, at least 4096
-        // tokens. Measured over split sizes 2048..24576, this picks the best or nearly the
-        // best one on c64_b16 (8192), long_c32 (8192) and the C5 c64 sweep (16384): fewer,
-        // longer items save per-item prologues and merge work until the last items to
-        // finish start to dominate. The host does not see the lengths themselves (they
-        // live on the device), so the bound uses max_kv_len.
+        // R * Hkv * max_kv_len head-tokens over 256 CUs, divided by 8, at least 2048
+        // tokens. Measured over split sizes 1024..24576, this picks the best or nearly the
+        // best one on c64_b16 (8192), long_c32 (8192), the C5 c64 sweep (16384) and the
+        // small rounds (2048 at 4..16 requests): fewer, longer items save per-item
+        // prologues and merge work until the last items to finish start to dominate, and
+        // below 2048 tokens the per-item costs outweigh the extra parallelism. The host
+        // does not see the lengths themselves (they live on the device), so the bound
+        // uses max_kv_len.
         long long want = (long long)d.num_reqs * d.num_kv_heads * d.max_kv_len / (256 * 8);
-        if (want < 4096) want = 4096;
+        if (want < 2048) want = 2048;
         split = (int)(((want + 63) / 64) * 64);
     }
     if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
