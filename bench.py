@@ -387,7 +387,8 @@ def main():
     x_bytes = accept_bytes(cfg, k)
     a_gbs = a_bytes / (t_attn * 1e-3) / 1e9
     x_gbs = x_bytes / (t_acc * 1e-3) / 1e9
-    log(f"step {ms_step:.3f} ms: budget {t_budget * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us "
+    log(f"step {ms_step:.3f} ms: budget {'given depths' if rnd.mode == 'given' else f'{t_budget * 1e3:.1f} us'}, "
+        f"attention {t_attn * 1e3:.1f} us "
         f"({a_gbs:.0f} GB/s), acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
 
     def post_step_figures():
@@ -517,7 +518,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": workload_text(cfg),
                    "concurrency": cfg.R, "block": cfg.b, "verified_positions": int(rnd.K),
-                   "verified_drafts": drafts, "budget_ratio_index": int(rnd.sel[1].item()),
+                   "verified_drafts": drafts,
+                   "budget_ratio_index": None if rnd.mode == "given" else int(rnd.sel[1].item()),
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (plan + split-KV attention + partial merge)",
                      "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
@@ -525,7 +527,8 @@ def main():
                      "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest(),
                      "measured_read_peak": read_gbs,
                      "frac_of_measured_read_peak": a_gbs / read_gbs if read_gbs else None},
-        "kernels": {"budget_us": t_budget * 1e3, "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
+        "kernels": {"budget_us": None if rnd.mode == "given" else t_budget * 1e3,
+                    "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
                     "acceptance_algorithmic_bytes": x_bytes,
                     **extra},
