@@ -2,16 +2,19 @@
 // acceptance probability min(1, p/q) whose expectation is the overlap of eq.
 // mtp-acceptance-tv).
 //
-// Four kernels on one stream:
+// Three kernels on one stream:
 //   rowstats  (logits mode only) streams every needed row once -- the n_i+1 target rows
 //             and n_i draft rows of each request -- and writes per-chunk (max, sum of
 //             exponentials). This is the HBM-bound pass.
-//   decide    one wavefront per request: merges the chunk statistics, evaluates the
+//   chunksum  per (request, vocabulary chunk). Its first wave takes the request's
+//             decision (decide_req): it merges the chunk statistics, evaluates the
 //             acceptance test of every draft in its own lane (exact fp64 product
-//             u*q < p), finds the first rejection with a ballot, writes the accepted
-//             prefix and the plan of the extra-token draw.
-//   chunksum  per (request, vocabulary chunk): the integer weights floor(r * 2^40) of the
-//             residual max(p - q, 0) (or of p for the bonus), summed over the chunk.
+//             u*q < p) and finds the first rejection with a ballot; the chunk-0
+//             workgroup writes the accepted prefix and the plan of the extra-token draw.
+//             Then the workgroup sums the integer weights floor(r * 2^40) of the
+//             residual max(p - q, 0) (or of p for the bonus) over its chunk. Every
+//             workgroup of a request computes the same decision from the same data, so
+//             no workgroup waits for another and one launch (and its gap) is saved.
 //   search    per request: Z, the threshold floor(m * Z / 2^24), the chunk holding it and
 //             the exact token inside that chunk.
 // Every sum that decides a token is an integer sum, so the result does not depend on
@@ -218,25 +221,28 @@ __device__ inline void merge_stats(const float2* st, int NC, float& m, float& iS
 }
 
 // ----------------------------------------------------------------------------------
-// decide: one wavefront per request
+// decision of request i, taken by one wavefront (lane = 0..63); the plan is valid in lane
+// 0. With write set, the accepted prefix, accept_len, flags of a malformed request and
+// the plan are stored.
 // ----------------------------------------------------------------------------------
 template <bool LOGITS, typename T>
-__global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
-    const int i = blockIdx.x, lane = threadIdx.x;
+__device__ inline ReqPlan decide_req(const AcceptArgs& a, const int i, const int lane, const bool write) {
     const int q0 = a.qo[i];
     const int n = a.qo[i + 1] - q0 - 1;
     const int K = a.qo[a.R];
     ReqPlan pl{};
     if (n < 0 || n > a.D || q0 < 0 || q0 + n + 1 > K || K > a.R * a.b) {  // malformed packing: nothing to draw
-        if (lane == 0) {
-            pl.mode = 2;
-            pl.flag = 2;
-            a.plan[i] = pl;
-            a.accept_len[i] = 0;
-            if (a.flags) a.flags[i] = 2;
+        pl.mode = 2;
+        pl.flag = 2;
+        if (write) {
+            if (lane == 0) {
+                a.plan[i] = pl;
+                a.accept_len[i] = 0;
+                if (a.flags) a.flags[i] = 2;
+            }
+            for (int t = lane; t < a.b; t += 64) a.out_tokens[(size_t)i * a.b + t] = -1;
         }
-        for (int t = lane; t < a.b; t += 64) a.out_tokens[(size_t)i * a.b + t] = -1;
-        return;
+        return pl;
     }
     // per-row softmax statistics: lane r -> P_r (r <= n), lane 32+t -> Q_{t+1} (t < n)
     float m = 0.0f, iS = 0.0f;
@@ -272,10 +278,11 @@ __global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
     const uint64_t fails = __ballot(reject);
     const int acc = fails ? __builtin_ctzll(fails) : n;
     const int badflag = __shfl((int)bad_tok, acc & 63, 64) ? 4 : 0;
-    for (int t = lane; t < a.b; t += 64) {
-        if (t < acc) a.out_tokens[(size_t)i * a.b + t] = a.tokens[(size_t)i * a.D + t];
-        else if (t > acc) a.out_tokens[(size_t)i * a.b + t] = -1;
-    }
+    if (write)
+        for (int t = lane; t < a.b; t += 64) {
+            if (t < acc) a.out_tokens[(size_t)i * a.b + t] = a.tokens[(size_t)i * a.D + t];
+            else if (t > acc) a.out_tokens[(size_t)i * a.b + t] = -1;
+        }
     // statistics of P_a (lane a) and Q_{a+1} (lane 32+a), gathered by every lane
     const float pm = __shfl(m, acc & 31, 64), piS = __shfl(iS, acc & 31, 64);
     const float qm = __shfl(m, 32 + (acc & 31), 64), qiS = __shfl(iS, 32 + (acc & 31), 64);
@@ -290,10 +297,14 @@ __global__ __launch_bounds__(64) void decide_kernel(AcceptArgs a) {
         pl.iSP = piS;
         pl.mQ = acc < n ? qm : 0.0f;
         pl.iSQ = acc < n ? qiS : 0.0f;
-        a.plan[i] = pl;
-        a.accept_len[i] = acc;
+        if (write) {
+            a.plan[i] = pl;
+            a.accept_len[i] = acc;
+        }
     }
+    return pl;
 }
+
 
 template <bool LOGITS>
 __device__ inline uint64_t weight_xy(const ReqPlan& pl, int col, float x, float y, float invT);
@@ -404,14 +415,20 @@ __device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
 }
 
 // ----------------------------------------------------------------------------------
-// chunk sums: flat grid of (request, chunk); each workgroup sums the integer residual (or
-// bonus) weights of one vocabulary chunk of one request
+// chunk sums: flat grid of (request, chunk); each workgroup takes the request's decision
+// (first wave), then sums the integer residual (or bonus) weights of one vocabulary chunk
 // ----------------------------------------------------------------------------------
 template <bool LOGITS, typename T>
 __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     __shared__ uint64_t red[kThreads / 64];
+    __shared__ ReqPlan s_pl;
     const int i = blockIdx.x / a.NCR, c = blockIdx.x % a.NCR, tid = threadIdx.x;  // flat grid: (request, chunk)
-    const ReqPlan pl = a.plan[i];
+    if (tid < 64) {
+        const ReqPlan p0 = decide_req<LOGITS, T>(a, i, tid, c == 0);
+        if (tid == 0) s_pl = p0;
+    }
+    __syncthreads();
+    const ReqPlan pl = s_pl;
     if (pl.mode == 2) return;
     const int beg = c * kResChunk, end = min(a.V, beg + kResChunk);
     const int lo = min(end, beg + tid * kResPer), hi = min(end, lo + kResPer);
@@ -846,7 +863,6 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         if (e != hipSuccess) return e;
     }
 #define SV_ACCEPT_PHASES(LG, TT)                                                                      \
-    hipLaunchKernelGGL((decide_kernel<LG, TT>), dim3(d.num_reqs), dim3(64), 0, stream, a);            \
     hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
                        dim3(kThreads), 0, stream, a);                                                 \
     hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
