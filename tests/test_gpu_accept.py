@@ -319,3 +319,57 @@ def test_greedy_ties_nan_ragged(dev, orc, V):
         g = gpu_greedy(dev, tgt, D, tokens, qo, kind, dtype)
         o = orc.accept_greedy(tgt, (R, D, V), tokens, qo, dtype=dtype)
         assert_exact(g, o)
+
+
+def test_large_shape_without_partials(dev, orc):
+    """16400 requests over a 8193-token vocabulary: the per-thread partial sums would exceed
+    their 64 MB cap (16400 x 2 chunks x 256 threads x 8 B), so the draw searches its chunk
+    by rescanning it. The last chunk holds a single token. Bit-exact in probs mode."""
+    rng = np.random.default_rng(13)
+    R, b, V = 16400, 2, 8193
+    assert R * ((V + 8191) // 8192) * 256 * 8 > 64 << 20
+    k = rng.integers(1, b + 1, size=R)
+    from paper_2607_25852_amd import synth
+    qo = synth.indptr_from_depths(k.astype(np.int32))
+    # uniform rows scaled to sum to about 1 (exact normalisation is not needed for parity)
+    target = rng.random((int(qo[-1]), V), dtype=np.float32)
+    target *= np.float32(2.0 / V)
+    draft = rng.random((R, b - 1, V), dtype=np.float32)
+    draft *= np.float32(2.0 / V)
+    tokens = rng.integers(0, V, size=(R, b - 1)).astype(np.int32)
+    ua = (rng.integers(0, 1 << 24, size=(R, b - 1)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept without partials", R, V)
+    g = gpu_accept(dev, target, draft, tokens, qo, ua, us, "probs", "f32")
+    o = orc.accept(target, draft, tokens, qo, ua, us, kind="probs", dtype="f32")
+    assert_exact(g, o)
+    assert np.any(g["out_tokens"][:, :] >= 8192)  # some draws land in the one-token chunk
+
+
+def test_largest_vocabulary_logits(dev, orc):
+    """bf16 logits over the largest vocabulary the library accepts (2^22 tokens: 512
+    residual chunks and 256 statistics chunks per row), ragged blocks of up to 4."""
+    from paper_2607_25852_amd import synth
+    rng = np.random.default_rng(14)
+    R, b, V = 3, 4, 1 << 22
+    D = b - 1
+    k = np.array([4, 1, 3], dtype=np.int32)
+    qo = synth.indptr_from_depths(k)
+    tl = (rng.standard_normal((int(qo[-1]), V), dtype=np.float32) * 4).astype(np.float32)
+    dl = (rng.standard_normal((R, D, V), dtype=np.float32) * 4).astype(np.float32)
+    for i in range(R):  # drafts close to their target rows, except request 2's second draft
+        n = k[i] - 1
+        dl[i, :n] = tl[qo[i]:qo[i] + n] + rng.standard_normal((n, V), dtype=np.float32)
+    tl, dl = synth.bf16_bits(tl), synth.bf16_bits(dl)
+    toks = np.stack([[int(np.argmax(dl[i, t])) if t % 2 == 0 else int(rng.integers(0, V)) for t in range(D)]
+                     for i in range(R)]).astype(np.int32)
+    # the drafted token's target logit far below its draft logit: rejected, residual draw
+    toks[2, 1] = int(np.argmin(synth.bf16_to_f32(tl[qo[2] + 1]) - synth.bf16_to_f32(dl[2, 1])))
+    ua = (rng.integers(0, 1 << 24, size=(R, D)) * 2.0 ** -24).astype(np.float32)
+    us = (rng.integers(0, 1 << 24, size=R) * 2.0 ** -24).astype(np.float32)
+    say("accept largest vocabulary", V)
+    g = gpu_accept(dev, tl, dl, toks, qo, ua, us, "logits", "bf16", 1.0)
+    o = orc.accept(tl, dl, toks, qo, ua, us, kind="logits", dtype="bf16", temperature=1.0, diagnostics=True)
+    exact, marginal, failures = classify_accept(g, o, ua)
+    assert not failures, failures[:5]
+    assert marginal <= 1
