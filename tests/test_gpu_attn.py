@@ -224,3 +224,39 @@ def test_wide_group_whole_tile_waves(dev, orc, page, d):
     # the same rows through several splits agree with the single-split result
     q2, kvl2, o2, l2 = run_gpu_attn(dev, cfg, kv, qo, L, kv_split=128)
     assert np.abs(o2 - o).max() <= 2e-2 and np.abs(l2 - l).max() <= 1e-3
+
+
+
+def test_longest_context(dev, orc):
+    """A request at the longest accepted context (2^22 tokens with its block, 65536 pages of
+    64): 2048 splits of 2048 tokens merged per row, next to a shorter request. The cache
+    holds random bf16 values of magnitude [0.5, 1) with random signs (cheap to generate at
+    this size) behind a shuffled page table."""
+    from paper_2607_25852_amd import synth
+    L = np.array([(1 << 22) - 4, 300001], np.int32)
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name="longest", R=2, b=4, dtype="bf16", Hq=8, Hkv=1, d=128,
+                              page=64, kv=("list",) + tuple(int(x) for x in L))
+    qo = synth.indptr_from_depths(np.array([4, 3], np.int32))
+    say("attn gen longest")
+    rng = np.random.default_rng(21)
+    need = [-(-(int(L[i]) + cfg.b) // cfg.page) for i in range(cfg.R)]
+    pool = sum(need)
+    perm = rng.permutation(pool).astype(np.int32)
+    pt = np.full((cfg.R, max(need)), -1, np.int32)
+    pt[0, :need[0]] = perm[:need[0]]
+    pt[1, :need[1]] = perm[need[0]:]
+
+    def cache():
+        bits = rng.integers(0, 1 << 16, size=(pool, cfg.Hkv, cfg.page, cfg.d), dtype=np.uint16)
+        return (bits & np.uint16(0x807F)) | np.uint16(0x3F00)
+
+    # queries scaled by 8: a few keys dominate each row, so a lost or misplaced split moves
+    # the output and the lse by O(1)
+    q32 = rng.standard_normal((cfg.R, cfg.b, cfg.Hq, cfg.d), dtype=np.float32) * np.float32(8.0)
+    kv = dict(q_full=synth.bf16_bits(q32), page_table=pt, num_pages=pool, k_cache=cache(), v_cache=cache())
+    say("attn run longest")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    assert int(kvl.max()) == 1 << 22
+    rows = np.array([0, 0, 3, 3, 4, 4, 5, 6], np.int32)
+    heads = np.array([0, 5, 2, 7, 1, 6, 3, 4], np.int32)
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=(rows, heads))
