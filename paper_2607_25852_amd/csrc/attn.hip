@@ -775,6 +775,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
             if (pg >= 0 && pg < a.num_pages) {
                 off = (((size_t)pg * a.Hkv + kvh) * P + (sk & (P - 1))) * HD;
                 float dot = 0.0f;
+#pragma unroll 4
                 for (int e = 0; e < HD; e += 4) {
                     const f32x4 kv4 = *(const f32x4*)(kcp + off + e);
                     dot += qp[e] * kv4[0] + qp[e + 1] * kv4[1] + qp[e + 2] * kv4[2] + qp[e + 3] * kv4[3];
@@ -794,16 +795,29 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
         l = l * alpha + ps;
         m = m_new;
         for (int e = 0; e < 4; e++) o[e] *= alpha;
+        // P V, keys in order; the V loads of 8 keys are issued before their products (keys
+        // outside the mask or on an invalid page are skipped, never multiplied)
         const int cnt = min(64, limit - base + 1);
-        for (int jj = 0; jj < cnt; jj++) {
-            const float pj = __shfl(p, jj, 64);
-            const int okj = __shfl((int)ok, jj, 64);
-            if (!okj) continue;
-            const size_t offj = __shfl((unsigned long long)off, jj, 64);
-            for (int e = 0; e < 4; e++) {
-                const int dd = lane + 64 * e;
-                if (dd < HD) o[e] += pj * vcp[offj + dd];
+        for (int j0 = 0; j0 < cnt; j0 += 8) {
+            float pj[8], vv[8][4];
+            bool okj[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int jj = j0 + u;
+                pj[u] = __shfl(p, jj & 63, 64);
+                okj[u] = __shfl((int)ok, jj & 63, 64) != 0 && jj < cnt;
+                const size_t offj = __shfl((unsigned long long)off, jj & 63, 64);
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    const int dd = lane + 64 * e;
+                    vv[u][e] = (okj[u] && dd < HD) ? vcp[offj + dd] : 0.0f;
+                }
             }
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                if (okj[u])
+#pragma unroll
+                    for (int e = 0; e < 4; e++) o[e] += pj[u] * vv[u][e];
         }
     }
     float* op = (float*)a.out + ((size_t)row * a.Hq + head) * HD;
