@@ -795,29 +795,35 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
         l = l * alpha + ps;
         m = m_new;
         for (int e = 0; e < 4; e++) o[e] *= alpha;
-        // P V, keys in order; the V loads of 8 keys are issued before their products (keys
-        // outside the mask or on an invalid page are skipped, never multiplied)
+        // P V, keys in order for every output element. The key index is uniform, so each
+        // key's p, mask bit and V row offset are broadcast with readlane (no LDS traffic), and
+        // the V loads of 32 keys are issued before their products. Keys outside the mask or
+        // on an invalid page are skipped, never multiplied.
         const int cnt = min(64, limit - base + 1);
-        for (int j0 = 0; j0 < cnt; j0 += 8) {
-            float pj[8], vv[8][4];
-            bool okj[8];
+        const uint32_t okmask_lo = (uint32_t)__ballot(ok), okmask_hi = (uint32_t)(__ballot(ok) >> 32);
+        const uint32_t off_lo = (uint32_t)off, off_hi = (uint32_t)(off >> 32);
 #pragma unroll
-            for (int u = 0; u < 8; u++) {
-                const int jj = j0 + u;
-                pj[u] = __shfl(p, jj & 63, 64);
-                okj[u] = __shfl((int)ok, jj & 63, 64) != 0 && jj < cnt;
-                const size_t offj = __shfl((unsigned long long)off, jj & 63, 64);
+        for (int e = 0; e < 4; e++) {
+            if (64 * e >= HD) break;
+            const int dd = lane + 64 * e;
+            const bool dok = dd < HD;
+            for (int j0 = 0; j0 < cnt; j0 += 32) {
+                float vv[32];
 #pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    const int dd = lane + 64 * e;
-                    vv[u][e] = (okj[u] && dd < HD) ? vcp[offj + dd] : 0.0f;
+                for (int u = 0; u < 32; u++) {
+                    const int jj = j0 + u;
+                    const bool okj = jj < cnt && (((jj < 32 ? okmask_lo >> jj : okmask_hi >> (jj - 32)) & 1u) != 0);
+                    const size_t offj = ((size_t)(uint32_t)__builtin_amdgcn_readlane((int)off_hi, jj & 63) << 32) |
+                                        (uint32_t)__builtin_amdgcn_readlane((int)off_lo, jj & 63);
+                    vv[u] = (okj && dok) ? vcp[offj + dd] : 0.0f;
+                }
+#pragma unroll
+                for (int u = 0; u < 32; u++) {
+                    const int jj = j0 + u;
+                    const bool okj = jj < cnt && (((jj < 32 ? okmask_lo >> jj : okmask_hi >> (jj - 32)) & 1u) != 0);
+                    if (okj) o[e] += __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, p), jj & 63)) * vv[u];
                 }
             }
-#pragma unroll
-            for (int u = 0; u < 8; u++)
-                if (okj[u])
-#pragma unroll
-                    for (int e = 0; e < 4; e++) o[e] += pj[u] * vv[u][e];
         }
     }
     float* op = (float*)a.out + ((size_t)row * a.Hq + head) * HD;
