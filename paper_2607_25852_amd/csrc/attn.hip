@@ -738,8 +738,12 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 // fp32 vector kernel: one wavefront per (query row, head); HD <= 256, HD % 4 == 0
 // ---------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
+    // one workgroup per (row, head); wave wv takes the 64-key tiles wv, wv + 4, ... and the
+    // four waves' softmax states are merged at the end
+    __shared__ float s_o[4][4][64];
+    __shared__ float s_ml[4][2];
     const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int unit = blockIdx.x * 4 + wv;
+    const int unit = blockIdx.x;
     const int K = a.qo[a.R];
     if (K > a.total_q) return;
     const int row = unit / a.Hq, head = unit % a.Hq;
@@ -764,7 +768,7 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
     const int P = 1 << a.log2P;
     float o[4] = {0.f, 0.f, 0.f, 0.f};
     float m = -INFINITY, l = 0.0f;
-    for (int base = 0; base <= limit; base += 64) {
+    for (int base = 64 * wv; base <= limit; base += 256) {
         const int sk = base + lane;
         float z = -INFINITY;
         size_t off = 0;
@@ -826,13 +830,34 @@ __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
             }
         }
     }
+    // merge the four waves' (m, l, o): weights exp(m_w - M) over M = max m_w
+#pragma unroll
+    for (int e = 0; e < 4; e++) s_o[wv][e][lane] = o[e];
+    if (lane == 0) {
+        s_ml[wv][0] = m;
+        s_ml[wv][1] = l;
+    }
+    __syncthreads();
+    if (wv != 0) return;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < 4; w++) M = fmaxf(M, s_ml[w][0]);
+    float lt = 0.0f, ot[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int w = 0; w < 4; w++) {
+        const float mw = s_ml[w][0];
+        const float wt = mw == -INFINITY ? 0.0f : expf(mw - M);
+        lt += s_ml[w][1] * wt;
+#pragma unroll
+        for (int e = 0; e < 4; e++) ot[e] += s_o[w][e][lane] * wt;
+    }
     float* op = (float*)a.out + ((size_t)row * a.Hq + head) * HD;
-    const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+    const float inv = lt > 0.0f ? 1.0f / lt : 0.0f;
     for (int e = 0; e < 4; e++) {
         const int dd = lane + 64 * e;
-        if (dd < HD) op[dd] = o[e] * inv;
+        if (dd < HD) op[dd] = ot[e] * inv;
     }
-    if (a.lse && lane == 0) a.lse[(size_t)row * a.Hq + head] = l > 0.0f ? m + logf(l) : -INFINITY;
+    if (a.lse && lane == 0) a.lse[(size_t)row * a.Hq + head] = lt > 0.0f ? M + logf(lt) : -INFINITY;
 }
 
 int ilog2(int x) {
@@ -926,7 +951,7 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
 
     if (d.dtype == SV_F32) {
         const int units = d.total_q_max * d.num_q_heads;
-        hipLaunchKernelGGL(attn_f32_kernel, dim3((units + 3) / 4), dim3(256), 0, stream, a, d.head_dim);
+        hipLaunchKernelGGL(attn_f32_kernel, dim3(units), dim3(256), 0, stream, a, d.head_dim);
         return hipGetLastError();
     }
     a.nrb = plan.row_blocks;
