@@ -13,7 +13,8 @@
 // at once; requests with more than one split write fp32 partials merged by a
 // second kernel (log-sum-exp weights).
 //
-// fp32 path (vector ALU): one wavefront per (query row, head), 64 keys per step.
+// fp32 path (vector ALU): one workgroup per (query row, head); its four waves take
+// interleaved 64-key tiles and merge their softmax states at the end.
 #include <atomic>
 
 #include "sv_internal.h"
@@ -735,7 +736,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 }
 
 // ---------------------------------------------------------------------------------
-// fp32 vector kernel: one wavefront per (query row, head); HD <= 256, HD % 4 == 0
+// fp32 vector kernel: one workgroup of four waves per (query row, head); HD <= 256, HD % 4 == 0
 // ---------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_f32_kernel(AttnArgs a, int HD) {
     // one workgroup per (row, head); wave wv takes the 64-key tiles wv, wv + 4, ... and the
