@@ -27,9 +27,10 @@
  *
  * Conventions shared by every entry point
  *   - All array pointers are caller-owned DEVICE memory unless marked "host".
- *     The library allocates nothing and keeps no state between calls; each call
- *     only enqueues kernels on `stream` (a hipStream_t; NULL = the default
- *     stream) and returns without waiting for them.
+ *     The library allocates nothing and keeps no state between calls (apart from
+ *     the fixed device scratch of sv_spec_accept_noalloc); each call only enqueues
+ *     kernels on `stream` (a hipStream_t; NULL = the default stream) and returns
+ *     without waiting for them.
  *   - Descriptors are host structs, read during the call only.
  *   - Alignment: the floating-point data arrays (q, caches, out, logits) and the
  *     workspaces must be 16-byte aligned; int32 and fp32 index / scalar arrays
@@ -280,6 +281,25 @@ sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const v
                          int32_t* out_tokens, int32_t* flags, void* ws, size_t ws_bytes,
                          void* stream);
 size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc);
+
+/*
+ * sv_spec_accept_noalloc -- sv_spec_accept without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Same arguments, kernels, results and errors as
+ * sv_spec_accept, minus ws / ws_bytes; the library allocates nothing.
+ * The workspace is a fixed 16 MiB device array inside the library, one per GPU, held from
+ * the first call on that GPU until the process ends. Shapes whose
+ * sv_spec_accept_workspace_size exceeds 16 MiB are rejected with SV_ERR_UNSUPPORTED
+ * (c64_b16-like rounds need about 2.3 MiB). Every call on a GPU uses that GPU's array and
+ * leaves its contents behind: calls that overlap on one GPU (different streams or host
+ * threads without ordering) race and give undefined results; order them, or use
+ * sv_spec_accept with separate workspaces. The array belongs to the device of `stream`
+ * (NULL: the current device).
+ */
+sv_status sv_spec_accept_noalloc(const sv_accept_desc* desc, const void* target, const void* draft,
+                                 const int32_t* draft_tokens, const int32_t* qo_indptr, const float* u_accept,
+                                 const float* u_sample, int32_t* accept_len, int32_t* out_tokens, int32_t* flags,
+                                 void* stream);
 
 /*
  * sv_spec_accept_stats -- sv_spec_accept (LOGITS, temperature > 0) with the draft rows'

@@ -22,7 +22,8 @@ SV_MAX_RATIOS = 8
 
 # every symbol the header declares (checked by the ABI test)
 EXPORTED = ("sv_alloc_budget", "sv_pack_verify", "sv_append_kv", "sv_verify_attn", "sv_verify_attn_workspace_size",
-            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_stats", "sv_draft_stats",
+            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_noalloc", "sv_spec_accept_stats",
+            "sv_draft_stats",
             "sv_draft_stats_workspace_size", "sv_status_string", "sv_last_error", "sv_abi_version")
 
 
@@ -92,6 +93,8 @@ def load() -> ctypes.CDLL:
     lib.sv_spec_accept.restype = i32
     lib.sv_spec_accept_workspace_size.argtypes = [ctypes.POINTER(AcceptDesc)]
     lib.sv_spec_accept_workspace_size.restype = ctypes.c_size_t
+    lib.sv_spec_accept_noalloc.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P]
+    lib.sv_spec_accept_noalloc.restype = i32
     lib.sv_spec_accept_stats.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P, P,
                                          ctypes.c_size_t, P]
     lib.sv_spec_accept_stats.restype = i32
@@ -254,6 +257,15 @@ def spec_accept(desc: AcceptDesc, target, draft, draft_tokens, qo_indptr, u_acce
     st = load().sv_spec_accept(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_tokens),
                                _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample), _ptr(accept_len),
                                _ptr(out_tokens), _ptr(flags), _ptr(ws), nbytes, _stream(stream))
+    _check(st)
+
+
+def spec_accept_noalloc(desc: AcceptDesc, target, draft, draft_tokens, qo_indptr, u_accept, u_sample, accept_len,
+                        out_tokens, flags=None, stream=None):
+    """sv_spec_accept_noalloc: the library's fixed device scratch replaces the workspace."""
+    st = load().sv_spec_accept_noalloc(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_tokens),
+                                       _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample), _ptr(accept_len),
+                                       _ptr(out_tokens), _ptr(flags), _stream(stream))
     _check(st)
 
 

@@ -1,6 +1,7 @@
 // Host side of libspecverify: argument validation, workspace sizing, launches and
 // error reporting for the C ABI declared in specverify.h. Every check runs before any
 // HIP call, so an invalid call enqueues nothing (and needs no GPU to be rejected).
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -249,12 +250,63 @@ size_t sv_spec_accept_workspace_size(const sv_accept_desc* desc) {
 
 namespace {
 
+// ---- the no-allocation acceptance entry point ---------------------------------------
+// A fixed device array stands in for the caller's workspace. Each GPU holds its own copy
+// (loaded with the code object, kept until the process ends). Its device address is
+// looked up once per device with hipGetSymbolAddress, with that device current; host code
+// never passes the array's own name to a kernel.
+constexpr size_t kScratchBytes = size_t(16) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// device address of `scratch` on the device that owns `stream` (NULL: the current device)
+sv_status scratch_for_stream(hipStream_t stream, void** out) {
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return fail(SV_ERR_HIP, "sv_spec_accept_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    int dev = cur;
+    if (stream) {
+        e = hipStreamGetDevice(stream, &dev);
+        if (e != hipSuccess)
+            return fail(SV_ERR_HIP, "sv_spec_accept_noalloc: hipStreamGetDevice: %s", hipGetErrorString(e));
+    }
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(SV_ERR_UNSUPPORTED, "sv_spec_accept_noalloc: device %d above %d", dev, kMaxDevices - 1);
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p) {
+        *out = p;
+        return SV_OK;
+    }
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess)
+        return fail(SV_ERR_HIP, "sv_spec_accept_noalloc: hipSetDevice: %s", hipGetErrorString(e));
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+        const hipError_t e2 = hipSetDevice(cur);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess || !p)
+        return fail(SV_ERR_HIP, "sv_spec_accept_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev].store(p, std::memory_order_release);  // racing first calls store the same address
+    *out = p;
+    return SV_OK;
+}
+
 sv_status spec_accept(const char* name, const sv_accept_desc* desc, const void* target, const void* draft,
                       const float* draft_stats, const int32_t* draft_tokens, const int32_t* qo_indptr,
                       const float* u_accept, const float* u_sample, int32_t* accept_len, int32_t* out_tokens,
-                      int32_t* flags, void* ws, size_t ws_bytes, void* stream) {
+                      int32_t* flags, void* ws, size_t ws_bytes, void* stream, bool use_scratch = false) {
     sv_status st = check_accept(desc);
     if (st != SV_OK) return st;
+    if (use_scratch) {  // the fixed device array takes the workspace's place
+        ws = nullptr;
+        ws_bytes = kScratchBytes;
+        if (sv::plan_accept(*desc).total > kScratchBytes)
+            return fail(SV_ERR_UNSUPPORTED,
+                        "%s: this shape needs %zu bytes of scratch, above the fixed %zu; use sv_spec_accept with a "
+                        "workspace",
+                        name, sv::plan_accept(*desc).total, kScratchBytes);
+    }
     const bool has_drafts = desc->block > 1;
     const bool greedy = desc->temperature == 0.0f;  // reads neither draft rows nor uniforms
     if (!target || !qo_indptr || !accept_len || !out_tokens || (has_drafts && !draft_tokens) ||
@@ -268,6 +320,7 @@ sv_status spec_accept(const char* name, const sv_accept_desc* desc, const void* 
                     "arrays 4-byte aligned",
                     name);
     const sv::AcceptPlan p = sv::plan_accept(*desc);
+    if (use_scratch && (st = scratch_for_stream((hipStream_t)stream, &ws)) != SV_OK) return st;
     if (!ws || ws_bytes < p.total)
         return fail(SV_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name, p.total,
                     ws ? ws_bytes : (size_t)0);
@@ -307,6 +360,14 @@ sv_status sv_spec_accept(const sv_accept_desc* desc, const void* target, const v
                          void* stream) {
     return spec_accept("sv_spec_accept", desc, target, draft, nullptr, draft_tokens, qo_indptr, u_accept, u_sample,
                        accept_len, out_tokens, flags, ws, ws_bytes, stream);
+}
+
+sv_status sv_spec_accept_noalloc(const sv_accept_desc* desc, const void* target, const void* draft,
+                                 const int32_t* draft_tokens, const int32_t* qo_indptr, const float* u_accept,
+                                 const float* u_sample, int32_t* accept_len, int32_t* out_tokens, int32_t* flags,
+                                 void* stream) {
+    return spec_accept("sv_spec_accept_noalloc", desc, target, draft, nullptr, draft_tokens, qo_indptr, u_accept,
+                       u_sample, accept_len, out_tokens, flags, nullptr, 0, stream, true);
 }
 
 sv_status sv_spec_accept_stats(const sv_accept_desc* desc, const void* target, const void* draft,

@@ -134,6 +134,22 @@ def test_accept_workspace_checks(lib):
     assert _accept(lib, d) == 1 and "NULL" in B.last_error()
 
 
+def test_accept_noalloc_host_checks(lib):
+    """The no-allocation variant rejects on the host, before any HIP call: a shape whose
+    workspace exceeds the fixed 16 MiB scratch, then NULL pointers."""
+    big = B.accept_desc(4096, 16, 131072, B.SV_LOGITS, B.SV_BF16)
+    assert lib.sv_spec_accept_workspace_size(ctypes.byref(big)) > 16 << 20
+    st = lib.sv_spec_accept_noalloc(ctypes.byref(big), None, None, None, None, None, None, None, None, None, None)
+    assert st == B.SV_ERR_UNSUPPORTED and "16777216" in B.last_error()
+    small = B.accept_desc(64, 16, 131072, B.SV_LOGITS, B.SV_BF16)
+    assert lib.sv_spec_accept_workspace_size(ctypes.byref(small)) <= 16 << 20
+    st = lib.sv_spec_accept_noalloc(ctypes.byref(small), None, None, None, None, None, None, None, None, None, None)
+    assert st == B.SV_ERR_INVALID_ARG and "NULL" in B.last_error()
+    bad = B.accept_desc(0, 16, 131072, B.SV_LOGITS, B.SV_BF16)
+    st = lib.sv_spec_accept_noalloc(ctypes.byref(bad), None, None, None, None, None, None, None, None, None, None)
+    assert st == B.SV_ERR_INVALID_ARG and "num_reqs" in B.last_error()
+
+
 def test_error_is_thread_local(lib):
     import threading
     d = B.accept_desc(0, 16, 100, B.SV_LOGITS, B.SV_F32)
