@@ -190,7 +190,8 @@ sv_status sv_append_kv(const sv_append_desc* desc, const void* k_new, const void
 /* ------------------------------------------------------------------------- */
 typedef struct {
     int32_t num_reqs;          /* R in [1, 65535]                                   */
-    int32_t total_q_max;       /* rows allocated in q / out / lse (>= qo_indptr[R])  */
+    int32_t total_q_max;       /* rows in q / out / lse: qo_indptr[R] <= it <= R*block,
+                                  and total_q_max * num_q_heads < 2^31                */
     int32_t block;             /* max k_i (<= 16)                                   */
     int32_t num_q_heads;       /* Hq                                               */
     int32_t num_kv_heads;      /* Hkv, Hq % Hkv == 0; G = Hq / Hkv                   */
@@ -300,6 +301,23 @@ sv_status sv_spec_accept_noalloc(const sv_accept_desc* desc, const void* target,
                                  const int32_t* draft_tokens, const int32_t* qo_indptr, const float* u_accept,
                                  const float* u_sample, int32_t* accept_len, int32_t* out_tokens, int32_t* flags,
                                  void* stream);
+
+/*
+ * sv_spec_accept_debug -- sv_spec_accept (LOGITS, temperature > 0) that also exports the
+ * fp32 values its decisions were taken on, so that a reference implementation of the
+ * acceptance rule (Sec. 1) applied to exactly those values can replay them:
+ *   dbg_pq  [2, R, b-1] fp32 out: [0][i][t-1] = P_{t-1}(d_t), [1][i][t-1] = Q_t(d_t) as
+ *           compared by the test of draft t (t = 1..n_i); other entries untouched;
+ *   dbg_row [R, 2, V] fp32 out: [i][0] = P_{a_i}(v), [i][1] = Q_{a_i+1}(v) (0 for a bonus
+ *           draw) as the residual weights of the draw use them; untouched for a malformed
+ *           request.
+ * The results are those of sv_spec_accept. A diagnostics call for tests: the export
+ * writes 8*R*V bytes more and is slower. Device memory owned by the caller.
+ */
+sv_status sv_spec_accept_debug(const sv_accept_desc* desc, const void* target, const void* draft,
+                               const int32_t* draft_tokens, const int32_t* qo_indptr, const float* u_accept,
+                               const float* u_sample, int32_t* accept_len, int32_t* out_tokens, int32_t* flags,
+                               float* dbg_pq, float* dbg_row, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * sv_spec_accept_stats -- sv_spec_accept (LOGITS, temperature > 0) with the draft rows'

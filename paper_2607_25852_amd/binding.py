@@ -22,7 +22,8 @@ SV_MAX_RATIOS = 8
 
 # every symbol the header declares (checked by the ABI test)
 EXPORTED = ("sv_alloc_budget", "sv_pack_verify", "sv_append_kv", "sv_verify_attn", "sv_verify_attn_workspace_size",
-            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_noalloc", "sv_spec_accept_stats",
+            "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_noalloc", "sv_spec_accept_debug",
+            "sv_spec_accept_stats",
             "sv_draft_stats",
             "sv_draft_stats_workspace_size", "sv_status_string", "sv_last_error", "sv_abi_version")
 
@@ -95,6 +96,9 @@ def load() -> ctypes.CDLL:
     lib.sv_spec_accept_workspace_size.restype = ctypes.c_size_t
     lib.sv_spec_accept_noalloc.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P]
     lib.sv_spec_accept_noalloc.restype = i32
+    lib.sv_spec_accept_debug.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P, P, P,
+                                         ctypes.c_size_t, P]
+    lib.sv_spec_accept_debug.restype = i32
     lib.sv_spec_accept_stats.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P, P,
                                          ctypes.c_size_t, P]
     lib.sv_spec_accept_stats.restype = i32
@@ -266,6 +270,17 @@ def spec_accept_noalloc(desc: AcceptDesc, target, draft, draft_tokens, qo_indptr
     st = load().sv_spec_accept_noalloc(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_tokens),
                                        _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample), _ptr(accept_len),
                                        _ptr(out_tokens), _ptr(flags), _stream(stream))
+    _check(st)
+
+
+def spec_accept_debug(desc: AcceptDesc, target, draft, draft_tokens, qo_indptr, u_accept, u_sample, accept_len,
+                      out_tokens, flags, dbg_pq, dbg_row, ws=None, stream=None):
+    """sv_spec_accept_debug: sv_spec_accept plus the fp32 values its decisions were taken on."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().sv_spec_accept_debug(ctypes.byref(desc), _ptr(target), _ptr(draft), _ptr(draft_tokens),
+                                     _ptr(qo_indptr), _ptr(u_accept), _ptr(u_sample), _ptr(accept_len),
+                                     _ptr(out_tokens), _ptr(flags), _ptr(dbg_pq), _ptr(dbg_row), _ptr(ws), nbytes,
+                                     _stream(stream))
     _check(st)
 
 

@@ -55,6 +55,8 @@ struct AcceptArgs {
     ReqPlan* plan;    // [R]
     uint64_t* csum;   // [R][NCR][2]
     uint64_t* tsum;   // [R][NCR][kThreads] per-thread partial sums of column 0, or NULL
+    float* dbg_pq;    // diagnostics or NULL: [2][R][D] the fp32 p(d_t), q(d_t) of every test
+    float* dbg_row;   // diagnostics: [R][2][V] the fp32 P_a(v), Q_{a+1}(v) the draw weighs
     int R, b, D, V, NC, stats_chunk, NCR, res_chunk;
     float invT;
 };
@@ -273,6 +275,10 @@ __device__ inline ReqPlan decide_req(const AcceptArgs& a, const int i, const int
             const float q = prob_of<LOGITS, T>(row_ptr<T>(a.draft, (long long)i * a.D + lane, a.V), d, mQt, iSQt, a.invT);
             const double u = (double)a.ua[(size_t)i * a.D + lane];
             reject = !(u * (double)q < (double)p);
+            if (write && a.dbg_pq) {  // diagnostics: the values this test compared
+                a.dbg_pq[(size_t)i * a.D + lane] = p;
+                a.dbg_pq[((size_t)a.R + i) * a.D + lane] = q;
+            }
         }
     }
     const uint64_t fails = __ballot(reject);
@@ -418,7 +424,26 @@ __device__ inline uint64_t block_sum_u64(uint64_t v, uint64_t* red) {
 // chunk sums: flat grid of (request, chunk); each workgroup takes the request's decision
 // (first wave), then sums the integer residual (or bonus) weights of one vocabulary chunk
 // ----------------------------------------------------------------------------------
+// diagnostics: the fp32 probabilities of the draw's row pair over [lo, hi), as the weights
+// of column 0 use them (the same expressions as weight_xy)
 template <bool LOGITS, typename T>
+__device__ inline void dbg_store_row(const AcceptArgs& a, const ReqPlan& pl, int i, int lo, int hi) {
+    const float c = a.invT * kLog2e;
+    const T* prow = row_ptr<T>(a.target, pl.rowP, a.V);
+    for (int v = lo; v < hi; v++) {
+        const float x = load_x<T>(prow, v);
+        const float pv = LOGITS ? __builtin_amdgcn_exp2f(__builtin_fmaf(x, c, -pl.mP * kLog2e)) * pl.iSP : x;
+        float qv = 0.0f;
+        if (pl.mode == 0) {
+            const float y = load_x<T>(row_ptr<T>(a.draft, pl.rowQ, a.V), v);
+            qv = LOGITS ? __builtin_amdgcn_exp2f(__builtin_fmaf(y, c, -pl.mQ * kLog2e)) * pl.iSQ : y;
+        }
+        a.dbg_row[((size_t)i * 2 + 0) * a.V + v] = pv;
+        a.dbg_row[((size_t)i * 2 + 1) * a.V + v] = qv;
+    }
+}
+
+template <bool LOGITS, typename T, bool DBG = false>
 __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     __shared__ uint64_t red[kThreads / 64];
     __shared__ ReqPlan s_pl;
@@ -440,6 +465,7 @@ __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
     } else {
         part = range_sum<LOGITS, T>(a, pl, 0, lo, hi);
     }
+    if (DBG) dbg_store_row<LOGITS, T>(a, pl, i, lo, hi);
     if (a.tsum) a.tsum[((size_t)i * a.NCR + c) * kThreads + tid] = part;
     const uint64_t sr = block_sum_u64(part, red);
     if (tid == 0) a.csum[((size_t)i * a.NCR + c) * 2 + 0] = sr;
@@ -817,7 +843,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
                          const void* draft, const float* draft_stats, const int32_t* draft_tokens,
                          const int32_t* qo_indptr, const float* u_accept, const float* u_sample,
                          int32_t* accept_len, int32_t* out_tokens, int32_t* flags, void* ws,
-                         hipStream_t stream) {
+                         hipStream_t stream, float* dbg_pq, float* dbg_row) {
     AcceptArgs a{};
     a.target = target;
     a.draft = draft;
@@ -829,6 +855,8 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     a.out_tokens = out_tokens;
     a.flags = flags;
     a.dstats = (const float2*)draft_stats;
+    a.dbg_pq = dbg_pq;
+    a.dbg_row = dbg_row;
     char* w = (char*)ws;
     a.stats_t = (float2*)(w + p.off_stats_t);
     a.stats_q = (float2*)(w + p.off_stats_q);
@@ -862,9 +890,13 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-#define SV_ACCEPT_PHASES(LG, TT)                                                                      \
-    hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
-                       dim3(kThreads), 0, stream, a);                                                 \
+#define SV_ACCEPT_PHASES(LG, TT)                                                                         \
+    if (dbg_row)                                                                                         \
+        hipLaunchKernelGGL((chunksum_kernel<LG, TT, true>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
+                           dim3(kThreads), 0, stream, a);                                                \
+    else                                                                                                 \
+        hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
+                           dim3(kThreads), 0, stream, a);                                                \
     hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
     if (logits && bf) {
         SV_ACCEPT_PHASES(true, uint16_t);

@@ -86,6 +86,14 @@ sv_status check_attn(const sv_attn_desc* d) {
     if (d->block < 1 || d->block > SV_MAX_BLOCK)
         return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: block %d outside [1, %d]", d->block, SV_MAX_BLOCK);
     if (d->total_q_max < 1) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: total_q_max %d < 1", d->total_q_max);
+    // the packed batch holds at most block rows per request, and the fp32 path launches one
+    // workgroup per (row, head): both products in 64 bits
+    if ((long long)d->total_q_max > (long long)d->num_reqs * d->block)
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: total_q_max %d above num_reqs*block = %lld", d->total_q_max,
+                    (long long)d->num_reqs * d->block);
+    if (d->num_q_heads > 0 && (long long)d->total_q_max * d->num_q_heads > 0x7FFFFFFFLL)
+        return fail(SV_ERR_UNSUPPORTED, "sv_verify_attn: total_q_max*num_q_heads = %lld above 2^31-1",
+                    (long long)d->total_q_max * d->num_q_heads);
     if (d->num_q_heads < 1 || d->num_kv_heads < 1 || d->num_q_heads % d->num_kv_heads != 0)
         return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: num_q_heads %d is not a multiple of num_kv_heads %d",
                     d->num_q_heads, d->num_kv_heads);
@@ -295,7 +303,8 @@ sv_status scratch_for_stream(hipStream_t stream, void** out) {
 sv_status spec_accept(const char* name, const sv_accept_desc* desc, const void* target, const void* draft,
                       const float* draft_stats, const int32_t* draft_tokens, const int32_t* qo_indptr,
                       const float* u_accept, const float* u_sample, int32_t* accept_len, int32_t* out_tokens,
-                      int32_t* flags, void* ws, size_t ws_bytes, void* stream, bool use_scratch = false) {
+                      int32_t* flags, void* ws, size_t ws_bytes, void* stream, bool use_scratch = false,
+                      float* dbg_pq = nullptr, float* dbg_row = nullptr) {
     sv_status st = check_accept(desc);
     if (st != SV_OK) return st;
     if (use_scratch) {  // the fixed device array takes the workspace's place
@@ -326,7 +335,8 @@ sv_status spec_accept(const char* name, const sv_accept_desc* desc, const void* 
                     ws ? ws_bytes : (size_t)0);
     if (inject_launch_fault()) return fail(SV_ERR_HIP, "%s: injected launch failure", name);
     return launched(sv::launch_accept(*desc, p, target, draft, draft_stats, draft_tokens, qo_indptr, u_accept,
-                                      u_sample, accept_len, out_tokens, flags, ws, (hipStream_t)stream),
+                                      u_sample, accept_len, out_tokens, flags, ws, (hipStream_t)stream, dbg_pq,
+                                      dbg_row),
                     name);
 }
 
@@ -368,6 +378,19 @@ sv_status sv_spec_accept_noalloc(const sv_accept_desc* desc, const void* target,
                                  void* stream) {
     return spec_accept("sv_spec_accept_noalloc", desc, target, draft, nullptr, draft_tokens, qo_indptr, u_accept,
                        u_sample, accept_len, out_tokens, flags, nullptr, 0, stream, true);
+}
+
+sv_status sv_spec_accept_debug(const sv_accept_desc* desc, const void* target, const void* draft,
+                               const int32_t* draft_tokens, const int32_t* qo_indptr, const float* u_accept,
+                               const float* u_sample, int32_t* accept_len, int32_t* out_tokens, int32_t* flags,
+                               float* dbg_pq, float* dbg_row, void* ws, size_t ws_bytes, void* stream) {
+    if (desc && (desc->kind != SV_LOGITS || !(desc->temperature > 0.0f)))
+        return fail(SV_ERR_INVALID_ARG,
+                    "sv_spec_accept_debug: the export covers rejection sampling of logits (LOGITS, temperature > 0)");
+    if (!dbg_pq || !dbg_row || !aligned(dbg_pq, 4) || !aligned(dbg_row, 4))
+        return fail(SV_ERR_INVALID_ARG, "sv_spec_accept_debug: dbg_pq and dbg_row must be 4-byte aligned device arrays");
+    return spec_accept("sv_spec_accept_debug", desc, target, draft, nullptr, draft_tokens, qo_indptr, u_accept,
+                       u_sample, accept_len, out_tokens, flags, ws, ws_bytes, stream, false, dbg_pq, dbg_row);
 }
 
 sv_status sv_spec_accept_stats(const sv_accept_desc* desc, const void* target, const void* draft,

@@ -47,7 +47,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const 
                          const void* draft, const float* draft_stats, const int32_t* draft_tokens,
                          const int32_t* qo_indptr, const float* u_accept, const float* u_sample,
                          int32_t* accept_len, int32_t* out_tokens, int32_t* flags, void* ws,
-                         hipStream_t stream);
+                         hipStream_t stream, float* dbg_pq = nullptr, float* dbg_row = nullptr);
 size_t draft_stats_workspace(const sv_draft_stats_desc& d);
 hipError_t launch_draft_stats(const sv_draft_stats_desc& d, const void* logits, float* stats, float* conf, void* ws,
                               hipStream_t stream);

@@ -86,6 +86,9 @@ def _attn(lib, d, ws_bytes=0):
     (dict(kv_split=100), 1, "kv_split"),
     (dict(max_pages_per_req=2), 1, "max_pages_per_req*page_size"),
     (dict(dtype=7), 1, "dtype"),
+    (dict(total_q_max=65), 1, "num_reqs*block"),  # more rows than R*block
+    # total_q_max * Hq would wrap in 32 bits (the fp32 path's grid of (row, head) units)
+    (dict(R=65535, block=16, total_q_max=65535 * 16, Hq=4096, Hkv=4096, d=64, dtype=B.SV_F32), 2, "2^31"),
 ])
 def test_attn_descriptor_checks(lib, kw, status, msg):
     base = dict(R=4, total_q_max=64, block=16, Hq=32, Hkv=8, d=128, page_size=64, max_pages_per_req=130,

@@ -3,16 +3,18 @@
 Gate: max-abs <= 2e-2 (bf16) / 1e-5 (fp32) plus relative RMS <= 1e-2 (bf16) /
 1e-5 (fp32) and |lse difference| <= 1e-3 / 1e-5 -- at 64K-128K keys the outputs
 shrink to ~1/sqrt(L), so the max-abs gate alone would pass an all-zero output.
-Small workloads are compared on every (row, head); full-size ones on sampled
-(row, head) units covering every request, the first and last block row and
-every kv-head group.
+The concurrency-64 round is compared on every (row, head) of the packing its own
+budget chooses (the attention the bench times), the long-context round on every
+(row, head) of eight whole requests, and every point of the concurrency sweep on the
+budget's packing: every unit up to 8 requests, otherwise sampled (row, head) units
+covering every request, the first and last block row and every kv-head group.
 """
 import dataclasses
 
 import numpy as np
 import pytest
 
-from gpu_util import bf16_bits_of, compare_attention, f32_of_bits, say
+from gpu_util import SWEEP, bf16_bits_of, budget_packing, compare_attention, f32_of_bits, say
 
 pytestmark = pytest.mark.gpu
 
@@ -76,25 +78,18 @@ def check(orc, cfg, kv, qo, kv_lens, q, o_gpu, lse_gpu, units=None, scale=None):
     return stats
 
 
-def _qo_for(cfg, orc=None):
+@pytest.mark.parametrize("page,d", [(16, 64), (1, 4), (64, 100), (1, 128), (64, 256), (16, 100)])
+def test_tiny_fp32_full(dev, orc, page, d):
+    """fp32 path at 1e-5: head dims from 4 to 256 (100: not a multiple of 64), pages of 1 to
+    64 tokens, NaN in every page and slot nobody owns, and a context of 4100 keys so that
+    each of the four waves walks many 64-key tiles."""
     from paper_2607_25852_amd import synth
-    import oracle
-    if cfg.budget[0] == "given":
-        return synth.indptr_from_depths(synth.given_depths(cfg))
-    conf = synth.make_logits_round(cfg)["conf"] if cfg.V <= 32768 else None
-    if cfg.budget[0] == "fixed":
-        return oracle.budget(conf, "fixed", fixed_budget=cfg.budget[1])["qo_indptr"]
-    rng = np.random.default_rng(cfg.seed)
-    return synth.indptr_from_depths(rng.integers(1, cfg.b + 1, size=cfg.R).astype(np.int32))
-
-
-def test_tiny_fp32_full(dev, orc):
-    from paper_2607_25852_amd import synth
-    cfg = synth.CONFIGS["tiny"]
+    cfg = dataclasses.replace(synth.CONFIGS["tiny"], name=f"tiny_f32_p{page}_d{d}", page=page, d=d,
+                              kv=("list", 37, 128, 255, 4100))
     L = synth.kv_context_lengths(cfg)
     kv = synth.make_kv(cfg, L, fill_unused=np.nan)
-    qo = _qo_for(cfg)
-    say("attn tiny fp32")
+    qo = synth.indptr_from_depths(np.array([8, 3, 1, 8]))
+    say("attn tiny fp32", page, d)
     q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
     check(orc, cfg, kv, qo, kvl, q, o, l)
 
@@ -118,7 +113,7 @@ def test_c16_b16_full(dev, orc):
     cfg = synth.CONFIGS["c16_b16"]
     L = synth.kv_context_lengths(cfg)
     kv = synth.make_kv(cfg, L, fill_unused=np.nan)
-    qo = _qo_for(cfg)
+    qo = budget_packing("c16_b16")
     say("attn c16_b16")
     q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
     rows = np.repeat(np.arange(int(qo[-1])), cfg.Hq).astype(np.int32)
@@ -126,17 +121,73 @@ def test_c16_b16_full(dev, orc):
     check(orc, cfg, kv, qo, kvl, q, o, l, units=(rows, heads))
 
 
-@pytest.mark.parametrize("name", ["c64_b16", "long_c32", "sweep_blk_c64", "sweep_mtp_c8"])
-def test_full_size_sampled(dev, orc, name):
+def all_units(qo, Hq, rows=None):
+    rows = np.arange(int(qo[-1])) if rows is None else np.asarray(rows)
+    return (np.repeat(rows, Hq).astype(np.int32), np.tile(np.arange(Hq), len(rows)).astype(np.int32))
+
+
+def test_c64_b16_every_unit_on_budget_packing(dev, orc):
+    """The attention the bench times: the concurrency-64 round on the packing its own budget
+    chooses (K = 512 of 1024 positions), every (row, head) against the oracle. The GPU
+    budget's packing is checked to be that same packing first."""
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd import synth
+    from gpu_util import conf_of
+    cfg = synth.CONFIGS["c64_b16"]
+    qo = budget_packing("c64_b16")
+    assert int(qo[-1]) == 512
+    conf = dev.from_numpy(np.ascontiguousarray(conf_of("c64_b16"))).cuda()
+    bd = B.budget_desc(cfg.R, cfg.b, "cost", ratios_pm=synth.PAPER_RATIOS_PM, cost=synth.profiled_cost(cfg.R, cfg.b))
+    keep = dev.empty(cfg.R, dtype=dev.int32, device="cuda")
+    qo_d = dev.empty(cfg.R + 1, dtype=dev.int32, device="cuda")
+    sel = dev.empty(2, dtype=dev.int32, device="cuda")
+    B.alloc_budget(bd, conf, keep, qo_d, sel)
+    np.testing.assert_array_equal(qo_d.cpu().numpy(), qo)
+    L = synth.kv_context_lengths(cfg)
+    say("attn gen c64_b16")
+    kv = synth.make_kv(cfg, L)
+    say("attn run c64_b16")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=all_units(qo, cfg.Hq))
+
+
+def test_long_c32_whole_requests(dev, orc):
+    """Long context (64K-128K keys, group 16): every (row, head) of eight whole requests,
+    among them the shortest and longest context and the smallest and largest block."""
+    from paper_2607_25852_amd import synth
+    cfg = synth.CONFIGS["long_c32"]
+    L = synth.kv_context_lengths(cfg)
+    qo = budget_packing("long_c32")
+    k = np.diff(qo)
+    pick = {int(np.argmin(L)), int(np.argmax(L)), int(np.argmin(k)), int(np.argmax(k))}
+    for i in np.random.default_rng(5).permutation(cfg.R):
+        if len(pick) == 8:
+            break
+        pick.add(int(i))
+    rows = np.concatenate([np.arange(qo[i], qo[i + 1]) for i in sorted(pick)])
+    say("attn gen long_c32")
+    kv = synth.make_kv(cfg, L)
+    say("attn run long_c32")
+    q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
+    check(orc, cfg, kv, qo, kvl, q, o, l, units=all_units(qo, cfg.Hq, rows))
+
+
+@pytest.mark.parametrize("name", SWEEP)
+def test_sweep_on_budget_packing(dev, orc, name):
+    """Every concurrency and drafter mode of the sweep (the split rule takes different
+    values across them), on the packing each round's budget chooses."""
     from paper_2607_25852_amd import synth
     cfg = synth.CONFIGS[name]
     L = synth.kv_context_lengths(cfg)
+    qo = budget_packing(name)
     say("attn gen", name)
     kv = synth.make_kv(cfg, L)
-    qo = _qo_for(cfg)
     say("attn run", name)
     q, kvl, o, l = run_gpu_attn(dev, cfg, kv, qo, L)
-    units = sample_units(qo, cfg.Hq, cfg.Hq // cfg.Hkv, 4, np.random.default_rng(1))
+    if cfg.R <= 8:
+        units = all_units(qo, cfg.Hq)
+    else:
+        units = sample_units(qo, cfg.Hq, cfg.Hq // cfg.Hkv, 8, np.random.default_rng(1))
     check(orc, cfg, kv, qo, kvl, q, o, l, units=units)
 
 

@@ -6,7 +6,7 @@ import os
 import numpy as np
 import pytest
 
-from gpu_util import say
+from gpu_util import SWEEP, conf_of, say
 
 pytestmark = pytest.mark.gpu
 
@@ -50,13 +50,12 @@ def assert_same(g, o):
     np.testing.assert_array_equal(g["utility"], o["utility"])
 
 
-@pytest.mark.parametrize("name", ["tiny", "c16_b16", "c64_b16", "sweep_mtp_c4", "sweep_mtp_c64",
-                                  "sweep_blk_c8", "sweep_blk_c64"])
+@pytest.mark.parametrize("name", ["tiny", "c16_b16", "c64_b16"] + SWEEP)
 def test_workload_budgets(dev, orc, name):
     from paper_2607_25852_amd import synth
     cfg = synth.CONFIGS[name]
     say("budget workload", name)
-    conf = synth.make_logits_round(cfg)["conf"]
+    conf = conf_of(name)
     if cfg.budget[0] == "fixed":
         g = gpu_budget(dev, conf, "fixed", fixed=cfg.budget[1])
         o = orc.budget(conf, "fixed", fixed_budget=cfg.budget[1])
