@@ -47,6 +47,8 @@ def _load():
     lib.oracle_attn.restype = i32
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = i32
+    lib.oracle_set_num_threads.argtypes = [i32]
+    lib.oracle_set_num_threads.restype = i32
     _lib = lib
     return lib
 
@@ -61,6 +63,11 @@ def _c(a, dtype):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> int:
+    """Threads of the oracle's parallel loops from now on; returns the new setting."""
+    return int(_load().oracle_set_num_threads(int(n)))
 
 
 def prefix_scores(conf: np.ndarray) -> np.ndarray:

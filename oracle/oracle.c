@@ -531,3 +531,15 @@ int oracle_num_threads(void) {
     return 1;
 #endif
 }
+
+/* Threads of the parallel loops above (the host baseline times 1 and all). n < 1
+ * leaves the setting unchanged. Returns the setting in force afterwards. */
+int oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}

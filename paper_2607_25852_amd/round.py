@@ -1,11 +1,18 @@
 """One draft-verify round on the GPU through libspecverify.
 
 `DeviceRound` owns the torch device buffers of a round (inputs already resident
-in HBM, outputs, workspaces) and issues the three C-ABI calls on one stream:
-sv_alloc_budget -> sv_verify_attn -> sv_spec_accept. It only moves data and
+in HBM, outputs, workspaces) and issues the C-ABI calls on one stream:
+sv_alloc_budget -> sv_pack_verify -> sv_verify_attn -> sv_spec_accept. It only moves data and
 marshals arguments; all arithmetic of the round runs in the library's kernels.
+
+The round is self-contained on the device: the budget writes qo_indptr, the packing
+call turns it and the committed context lengths into the key counts kv_lens = L_i + k_i
+that attention reads, and acceptance reads the same qo_indptr. No per-round value
+crosses to the host between the calls.
 """
 from __future__ import annotations
+
+import copy
 
 import numpy as np
 import torch
@@ -73,17 +80,42 @@ class DeviceRound:
             torch.cuda.synchronize()
             self.qo_host = self.qo.cpu().numpy()
         self.K = int(self.qo_host[-1])
-        k = np.diff(self.qo_host)
+        # ---- packing inputs: the committed context lengths and each request's block
+        # (position 0 the certain token, then the drafts)
+        self.ctx_lens = to_dev(np.asarray(self.L, np.int32), device=device)
+        tok_rng = np.random.default_rng(cfg.seed + 17)
+        blk = np.empty((R, b), np.int32)
+        blk[:, 0] = tok_rng.integers(0, cfg.V, size=R)
+        if self.lr is not None and b > 1:
+            blk[:, 1:] = self.lr["draft_tokens"]
+        elif b > 1:
+            blk[:, 1:] = tok_rng.integers(0, cfg.V, size=(R, b - 1))
+        self.block_tokens_host = blk
+        self.block_tokens = to_dev(blk, device=device)
+        self.pdesc = B.pack_desc(R, b, R * b)
+        self.v_tokens = torch.empty(R * b, dtype=torch.int32, device=device)
+        self.v_positions = torch.empty(R * b, dtype=torch.int32, device=device)
+        self.kv_lens = torch.empty(R, dtype=torch.int32, device=device)
+        self.run_pack()
         # ---- attention inputs (cache holds L_i + b tokens; k_i of the block are visible)
         self.with_attn = with_attn
         if with_attn:
-            self.kv = kv if kv is not None else synth.make_kv(cfg, self.L, fill_unused=fill_unused)
-            self.kv_lens_host = (self.L + k).astype(np.int32)
+            on_device = isinstance(kv, str) and kv == "device"
+            if on_device:
+                self.kv = synth.make_kv(cfg, self.L, want_cache=False)
+            else:
+                self.kv = kv if kv is not None else synth.make_kv(cfg, self.L, fill_unused=fill_unused)
             self.q = to_dev(synth.pack_rows(self.kv["q_full"], self.qo_host), device=device)
-            self.k_cache = to_dev(self.kv["k_cache"], device=device)
-            self.v_cache = to_dev(self.kv["v_cache"], device=device)
+            if on_device:
+                g = torch.Generator(device=device)
+                g.manual_seed(cfg.seed)
+                shape = (self.kv["num_pages"], cfg.Hkv, cfg.page, cfg.d)
+                self.k_cache = torch.randn(shape, generator=g, dtype=dt_t, device=device)
+                self.v_cache = torch.randn(shape, generator=g, dtype=dt_t, device=device)
+            else:
+                self.k_cache = to_dev(self.kv["k_cache"], device=device)
+                self.v_cache = to_dev(self.kv["v_cache"], device=device)
             self.page_table = to_dev(self.kv["page_table"], device=device)
-            self.kv_lens = to_dev(self.kv_lens_host, device=device)
             pt = self.kv["page_table"]
             self.adesc = B.attn_desc(R, R * b, b, cfg.Hq, cfg.Hkv, cfg.d, cfg.page, pt.shape[1],
                                      self.kv["num_pages"], int(self.L.max()) + b,
@@ -119,11 +151,33 @@ class DeviceRound:
             self.flags = torch.empty(R, dtype=torch.int32, device=device)
             self.acc_ws = torch.empty(B.accept_workspace_size(self.xdesc), dtype=torch.uint8, device=device)
 
-    # ---- the three calls
+    def replica(self) -> "DeviceRound":
+        """Another copy of this round: every device buffer cloned (aliases kept), host
+        arrays shared. Copies used in turn make every step read its inputs from HBM
+        rather than from the last-level cache."""
+        r = copy.copy(self)
+        seen = {}
+        for name, v in vars(self).items():
+            if isinstance(v, torch.Tensor):
+                if id(v) not in seen:
+                    seen[id(v)] = v.clone()
+                setattr(r, name, seen[id(v)])
+        return r
+
+    def device_bytes(self) -> int:
+        """Bytes of the distinct device buffers of this round."""
+        seen = {id(v): v for v in vars(self).values() if isinstance(v, torch.Tensor)}
+        return int(sum(v.numel() * v.element_size() for v in seen.values()))
+
+    # ---- the calls
     def run_budget(self, stream=None):
         if self.mode == "given":
             return
         B.alloc_budget(self.bdesc, self.conf, self.keep, self.qo, self.sel, self.scores, self.util, stream)
+
+    def run_pack(self, stream=None):
+        B.pack_verify(self.pdesc, self.block_tokens, self.ctx_lens, self.qo, self.v_tokens, self.v_positions,
+                      self.kv_lens, stream)
 
     def run_attn(self, stream=None):
         B.verify_attn(self.adesc, self.q, self.k_cache, self.v_cache, self.page_table, self.qo, self.kv_lens,
@@ -135,6 +189,7 @@ class DeviceRound:
 
     def run(self, stream=None):
         self.run_budget(stream)
+        self.run_pack(stream)
         if self.with_attn:
             self.run_attn(stream)
         if self.with_accept:
