@@ -2,21 +2,24 @@
 // acceptance probability min(1, p/q) whose expectation is the overlap of eq.
 // mtp-acceptance-tv).
 //
-// Three kernels on one stream:
-//   rowstats  (logits mode only) streams every needed row once -- the n_i+1 target rows
-//             and n_i draft rows of each request -- and writes per-chunk (max, sum of
-//             exponentials). This is the HBM-bound pass.
-//   chunksum  per (request, vocabulary chunk). Its first wave takes the request's
+// Logits mode, two kernels on one stream, neither of which waits for another workgroup:
+//   rowstats  streams every needed row once -- the n_i+1 target rows and n_i draft rows
+//             of each request -- and writes per-chunk (max, sum of exponentials). This
+//             is the HBM-bound pass.
+//   draw      per (request, vocabulary chunk). Its first wave takes the request's
 //             decision (decide_req): it merges the chunk statistics, evaluates the
 //             acceptance test of every draft in its own lane (exact fp64 product
 //             u*q < p) and finds the first rejection with a ballot; the chunk-0
-//             workgroup writes the accepted prefix and the plan of the extra-token draw.
-//             Then the workgroup sums the integer weights floor(r * 2^40) of the
-//             residual max(p - q, 0) (or of p for the bonus) over its chunk. Every
-//             workgroup of a request computes the same decision from the same data, so
-//             no workgroup waits for another and one launch (and its gap) is saved.
-//   search    per request: Z, the threshold floor(m * Z / 2^24), the chunk holding it and
-//             the exact token inside that chunk.
+//             workgroup writes the accepted prefix. Every workgroup of a request
+//             computes the same decision from the same data, so none waits for another.
+//             The workgroup then sums the integer weights floor(r * 2^40) of the
+//             residual max(p - q, 0) (or of p for the bonus) over its chunk, stores the
+//             sum device-coherently and counts itself on the request's arrival counter;
+//             the last chunk workgroup of the request finds the token: Z, the threshold
+//             floor(m * Z / 2^24), the chunk holding it and the exact token inside it.
+// The arrival counters need no clearing launch: the statistics pass zeroes them.
+// Probability mode has no statistics pass: the chunk-sum kernel takes the decision and
+// sums the chunk, and a separate search kernel draws the token.
 // Every sum that decides a token is an integer sum, so the result does not depend on
 // how the vocabulary is split across threads.
 #include "sv_internal.h"
@@ -55,6 +58,7 @@ struct AcceptArgs {
     ReqPlan* plan;    // [R]
     uint64_t* csum;   // [R][NCR][2]
     uint64_t* tsum;   // [R][NCR][kThreads] per-thread partial sums of column 0, or NULL
+    uint32_t* cnt;    // [R][kCntStride] arrival counts of the draw's chunk workgroups (logits mode)
     float* dbg_pq;    // diagnostics or NULL: [2][R][D] the fp32 p(d_t), q(d_t) of every test
     float* dbg_row;   // diagnostics: [R][2][V] the fp32 P_a(v), Q_{a+1}(v) the draw weighs
     int R, b, D, V, NC, stats_chunk, NCR, res_chunk;
@@ -106,6 +110,27 @@ template <typename T>
 __device__ inline const T* row_ptr(const void* base, long long row, int V) {
     return (const T*)base + row * (long long)V;
 }
+
+// Values handed from one workgroup to another inside a kernel go through device-coherent
+// 8-byte stores and loads (agent scope: the XCDs' L2 caches are not coherent with each
+// other). A writer waits for its stores to complete before it counts itself on an
+// arrival counter, so the workgroup that sees the last count reads complete values.
+__device__ inline void store_dev(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline uint64_t load_dev(const uint64_t* p) {
+    return __hip_atomic_load((uint64_t*)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// wait until every store this wave issued has completed (stores count in vmcnt on gfx9)
+__device__ inline void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ inline uint32_t arrive(uint32_t* ctr) {
+    return __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Arrival counter of request i's draw: alone in a 128-byte cache line, because atomics
+// on one line are serialised and a request's workgroups arrive close together.
+constexpr int kCntStride = 32;  // uint32 per request
+__device__ inline size_t cnt_draw(int i) { return (size_t)i * kCntStride; }
 
 // (max, sum of 2^((x - max) log2e)) of x = l * invT over the chunk [beg, end) of one row,
 // valid in thread 0: every 16-byte load of the chunk is issued before any arithmetic
@@ -161,13 +186,15 @@ __device__ inline float2 chunk_stats(const T* row, int beg, int end, int V, int 
 
 // ----------------------------------------------------------------------------------
 // rowstats: flat grid of (row slot, chunk), R*b + R*D slots of NC chunks (R*b when the
-// draft rows' statistics are given)
+// draft rows' statistics are given): the packed target rows in order, then each
+// request's draft rows. Its first R workgroups also zero the draw's arrival counters.
 // ----------------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kThreads) void rowstats_kernel(AcceptArgs a) {
     __shared__ float red[kThreads / 64];
     const int slot = blockIdx.x / a.NC, c = blockIdx.x % a.NC;  // flat grid: (row slot, chunk)
     const int RB = a.R * a.b;
+    if (blockIdx.x < (unsigned)a.R && threadIdx.x == 0) a.cnt[cnt_draw(blockIdx.x)] = 0;
     const T* row;
     float2* dst;
     if (slot < RB) {
@@ -472,26 +499,26 @@ __global__ __launch_bounds__(kThreads) void chunksum_kernel(AcceptArgs a) {
 }
 
 // ----------------------------------------------------------------------------------
-// search: one workgroup per request. Z = sum of the chunk sums, the threshold
+// search of request i by one whole workgroup: Z = sum of the chunk sums, the threshold
 // floor(m * Z / 2^24), the chunk holding it (wave scan), then the token inside that chunk
 // (per-thread ranges, block scan, and the owning thread's scan of its loaded values).
-// An empty residual falls back to the weights of P_a, summed here (rare).
+// An empty residual falls back to the weights of P_a, summed here (rare). COH: the chunk
+// sums and partial sums come from other workgroups of the running kernel.
 // ----------------------------------------------------------------------------------
-template <bool LOGITS, typename T>
-__global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
+template <bool LOGITS, typename T, bool COH>
+__device__ inline void search_req(const AcceptArgs& a, const int i, const ReqPlan& pl) {
     __shared__ uint64_t red[kThreads / 64];
     __shared__ uint64_t wsum[kThreads / 64];
     __shared__ int s_chunk, s_token;
     __shared__ uint64_t s_before;
-    const int i = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const ReqPlan pl = a.plan[i];
-    if (pl.mode == 2) return;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int per = kResPer;
     // chunk sums: thread k < NCR keeps csum[k] in a register (wave 0 scans them below when
     // there are at most 64 chunks)
     uint64_t Z = 0, my_cs = 0;
     for (int k = tid; k < a.NCR; k += kThreads) {
-        const uint64_t v = a.csum[((size_t)i * a.NCR + k) * 2 + 0];
+        const uint64_t* src = a.csum + ((size_t)i * a.NCR + k) * 2;
+        const uint64_t v = COH ? load_dev(src) : *src;
         if (k == tid) my_cs = v;
         Z += v;
     }
@@ -528,8 +555,8 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
             int found = -1;
             for (int c0 = 0; c0 < a.NCR && found < 0; c0 += 64) {
                 const int k = c0 + lane;
-                const uint64_t v = k >= a.NCR ? 0 : (col == 0 && a.NCR <= 64) ? my_cs
-                                                             : a.csum[((size_t)i * a.NCR + k) * 2 + col];
+                const uint64_t* src = a.csum + ((size_t)i * a.NCR + k) * 2 + col;
+                const uint64_t v = k >= a.NCR ? 0 : (col == 0 && a.NCR <= 64) ? my_cs : COH ? load_dev(src) : *src;
                 const uint64_t incl = base + wave_incl_scan_u64(v, lane);
                 const bool hit = k < a.NCR && v > 0 && incl - v <= thr && thr < incl;
                 const uint64_t m = __ballot(hit);
@@ -556,7 +583,7 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
                 const uint64_t* ts = a.tsum + ((size_t)i * a.NCR + cs) * kThreads;
                 uint64_t v4[kThreads / 64];
 #pragma unroll
-                for (int k = 0; k < kThreads / 64; k++) v4[k] = ts[k * 64 + lane];
+                for (int k = 0; k < kThreads / 64; k++) v4[k] = COH ? load_dev(ts + k * 64 + lane) : ts[k * 64 + lane];
                 uint64_t base = 0, before = 0;
                 int found = -1;
 #pragma unroll
@@ -641,6 +668,56 @@ __global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
         a.out_tokens[(size_t)i * a.b + pl.a] = token;
         if (a.flags) a.flags[i] = flag;
     }
+}
+
+// search: one workgroup per request (probability mode)
+template <bool LOGITS, typename T>
+__global__ __launch_bounds__(kThreads) void search_kernel(AcceptArgs a) {
+    const ReqPlan pl = a.plan[blockIdx.x];
+    if (pl.mode == 2) return;
+    search_req<LOGITS, T, false>(a, blockIdx.x, pl);
+}
+
+// ----------------------------------------------------------------------------------
+// draw (logits mode): flat grid of (request, chunk). The first wave takes the request's
+// decision (the chunk-0 workgroup writes its outputs). The workgroup sums the residual
+// (or bonus) weights of its chunk, stores the sum and its threads' partial sums
+// device-coherently and counts itself; the request's last chunk workgroup runs the
+// search.
+// ----------------------------------------------------------------------------------
+template <typename T, bool DBG = false>
+__global__ __launch_bounds__(kThreads) void draw_kernel(AcceptArgs a) {
+    __shared__ uint64_t red[kThreads / 64];
+    __shared__ ReqPlan s_pl;
+    __shared__ int s_last;
+    const int i = blockIdx.x / a.NCR, c = blockIdx.x % a.NCR, tid = threadIdx.x;  // flat grid: (request, chunk)
+    if (tid < 64) {
+        const ReqPlan p0 = decide_req<true, T>(a, i, tid, c == 0);
+        if (tid == 0) s_pl = p0;
+    }
+    __syncthreads();
+    const ReqPlan pl = s_pl;
+    if (pl.mode == 2) return;
+    const int beg = c * kResChunk, end = min(a.V, beg + kResChunk);
+    const int lo = min(end, beg + tid * kResPer), hi = min(end, lo + kResPer);
+    uint64_t part;
+    if (range_is_full<T>(a, lo, hi)) {
+        RangeRegs<T> g;
+        range_load<T>(a, pl, 0, lo, g);
+        part = range_regs_sum<true, T>(a, pl, 0, g);
+    } else {
+        part = range_sum<true, T>(a, pl, 0, lo, hi);
+    }
+    if (DBG) dbg_store_row<true, T>(a, pl, i, lo, hi);
+    if (a.tsum) store_dev(a.tsum + ((size_t)i * a.NCR + c) * kThreads + tid, part);
+    const uint64_t sr = block_sum_u64(part, red);
+    if (tid == 0) store_dev(a.csum + ((size_t)i * a.NCR + c) * 2, sr);
+    wait_stores();
+    __syncthreads();
+    if (tid == 0) s_last = arrive(a.cnt + cnt_draw(i)) + 1 == (uint32_t)a.NCR;
+    __syncthreads();
+    if (!s_last) return;
+    search_req<true, T, true>(a, i, pl);
 }
 
 // ----------------------------------------------------------------------------------
@@ -824,6 +901,8 @@ AcceptPlan plan_accept(const sv_accept_desc& d) {
     const size_t R = d.num_reqs, b = d.block, D = b > 1 ? b - 1 : 1;
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     size_t off = 0;
+    p.off_cnt = off;
+    off = al(off + R * kCntStride * sizeof(uint32_t));
     p.off_stats_t = off;
     off = al(off + R * b * p.stats_chunks * sizeof(float2));
     p.off_stats_q = off;
@@ -863,6 +942,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     a.plan = (ReqPlan*)(w + p.off_plan);
     a.csum = (uint64_t*)(w + p.off_csum);
     a.tsum = p.off_tsum ? (uint64_t*)(w + p.off_tsum) : nullptr;
+    a.cnt = (uint32_t*)(w + p.off_cnt);
     a.R = d.num_reqs;
     a.b = d.block;
     a.D = d.block - 1;
@@ -881,6 +961,7 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         hipLaunchKernelGGL(decide_greedy_kernel, dim3(d.num_reqs), dim3(64), 0, stream, a);
         return hipGetLastError();
     }
+    const dim3 gres((unsigned)((long long)p.res_chunks * d.num_reqs));
     if (logits) {
         const long long slots = (long long)d.num_reqs * d.block +
                                 (draft_stats ? 0LL : (long long)d.num_reqs * (d.block > 1 ? d.block - 1 : 0));
@@ -889,23 +970,14 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
         else hipLaunchKernelGGL(rowstats_kernel<float>, g, dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        if (bf && dbg_row) hipLaunchKernelGGL((draw_kernel<uint16_t, true>), gres, dim3(kThreads), 0, stream, a);
+        else if (bf) hipLaunchKernelGGL((draw_kernel<uint16_t>), gres, dim3(kThreads), 0, stream, a);
+        else if (dbg_row) hipLaunchKernelGGL((draw_kernel<float, true>), gres, dim3(kThreads), 0, stream, a);
+        else hipLaunchKernelGGL((draw_kernel<float>), gres, dim3(kThreads), 0, stream, a);
+        return hipGetLastError();
     }
-#define SV_ACCEPT_PHASES(LG, TT)                                                                         \
-    if (dbg_row)                                                                                         \
-        hipLaunchKernelGGL((chunksum_kernel<LG, TT, true>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
-                           dim3(kThreads), 0, stream, a);                                                \
-    else                                                                                                 \
-        hipLaunchKernelGGL((chunksum_kernel<LG, TT>), dim3((unsigned)((long long)p.res_chunks * d.num_reqs)), \
-                           dim3(kThreads), 0, stream, a);                                                \
-    hipLaunchKernelGGL((search_kernel<LG, TT>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a)
-    if (logits && bf) {
-        SV_ACCEPT_PHASES(true, uint16_t);
-    } else if (logits) {
-        SV_ACCEPT_PHASES(true, float);
-    } else {
-        SV_ACCEPT_PHASES(false, float);
-    }
-#undef SV_ACCEPT_PHASES
+    hipLaunchKernelGGL((chunksum_kernel<false, float>), gres, dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((search_kernel<false, float>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

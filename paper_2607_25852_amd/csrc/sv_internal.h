@@ -40,7 +40,7 @@ struct AcceptPlan {
     int stats_chunks;  // chunks per row
     int res_chunk;     // vocabulary elements per residual workgroup
     int res_chunks;
-    size_t off_stats_t, off_stats_q, off_plan, off_csum, off_tsum, total;  // off_tsum 0: none
+    size_t off_cnt, off_stats_t, off_stats_q, off_plan, off_csum, off_tsum, total;  // off_tsum 0: none
 };
 AcceptPlan plan_accept(const sv_accept_desc& d);
 hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const void* target,

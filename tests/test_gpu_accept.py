@@ -221,6 +221,39 @@ def test_repeatable_bitwise(dev):
     assert_exact(a, b)
 
 
+@pytest.mark.parametrize("name,fill", [("tiny", 0xFF), ("c64_b16", 0xFF), ("c64_b16", 0x01), ("sweep_mtp_c16", 0x7F)])
+def test_workspace_contents_on_entry(dev, orc, name, fill):
+    """Logits mode counts the draw's chunk workgroups on per-request arrival counters in the
+    workspace, which the statistics pass zeroes first: whatever the workspace holds on
+    entry (here every byte set to `fill`), the outputs equal the oracle's, and a second
+    call on the same workspace gives the same outputs bit for bit."""
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd.round import to_dev
+    say("accept workspace fill", name, hex(fill))
+    cfg, target, draft, toks, qo, ua, us, dtype = _workload(name, "logits")
+    target, draft = poisoned(target, draft, qo)
+    R, D, V = draft.shape
+    d = B.accept_desc(R, D + 1, V, B.SV_LOGITS, B.SV_F32 if dtype == "f32" else B.SV_BF16, 1.0)
+    ws = dev.full((B.accept_workspace_size(d),), fill, dtype=dev.uint8, device="cuda")
+    tg, dr = to_dev(target), to_dev(draft)
+    tk, qd = to_dev(np.ascontiguousarray(toks, np.int32)), to_dev(np.ascontiguousarray(qo, np.int32))
+    uad, usd = to_dev(np.ascontiguousarray(ua, np.float32)), to_dev(np.ascontiguousarray(us, np.float32))
+    outs = []
+    for _ in range(2):
+        acc = dev.full((R,), -9, dtype=dev.int32, device="cuda")
+        out = dev.full((R, D + 1), -9, dtype=dev.int32, device="cuda")
+        flags = dev.full((R,), -9, dtype=dev.int32, device="cuda")
+        B.spec_accept(d, tg, dr, tk, qd, uad, usd, acc, out, flags, ws)
+        dev.cuda.synchronize()
+        outs.append(dict(accept_len=acc.cpu().numpy(), out_tokens=out.cpu().numpy(), flags=flags.cpu().numpy()))
+    assert_exact(outs[1], outs[0])
+    o = orc.accept(target[:int(qo[-1])], draft, toks, qo, ua, us, kind="logits", dtype=dtype, diagnostics=True)
+    exact, marginal, failures = classify_accept(outs[0], o, ua)
+    say("accept workspace fill", name, hex(fill), "exact", exact, "marginal", marginal, "fail", len(failures))
+    assert not failures, failures[:5]
+    assert marginal <= max(1, cfg.R // 50)
+
+
 def test_many_requests_flat_grids(dev, orc):
     """70000 requests of block 2 (more row slots than one grid dimension holds):
     the flat grids of both kernels still cover every request, bit-exact in probs mode."""
