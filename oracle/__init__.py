@@ -19,7 +19,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# SV_ORACLE_LIB names another build of oracle.c (the sanitizer test loads an
+# AddressSanitizer/UndefinedBehaviorSanitizer build through it)
+_LIB_PATH = os.environ.get("SV_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 

@@ -21,7 +21,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["sv_api.cpp", "budget.hip", "accept.hip", "attn.hip", "pack.hip"]
+SOURCES = ["sv_api.cpp", "sv_host.cpp", "budget.hip", "accept.hip", "attn.hip", "pack.hip"]
 PROBE_SOURCES = ["read_probe.hip"]
 COMMON = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-I" + INC, "-I" + CSRC,
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall", "-Wno-unused-function"]
@@ -43,9 +43,9 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def _link(objs, lib: str, verbose: bool) -> None:
+def _link(objs, lib: str, verbose: bool, libs=()) -> None:
     tmp = lib + ".tmp"
-    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs + list(libs)
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
@@ -56,7 +56,7 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     with ThreadPoolExecutor(max_workers=4) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES + PROBE_SOURCES))
-    _link(objs[:len(SOURCES)], LIB, verbose)
+    _link(objs[:len(SOURCES)], LIB, verbose, ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx"])
     _link(objs[len(SOURCES):], PROBE_LIB, verbose)
     return LIB
 

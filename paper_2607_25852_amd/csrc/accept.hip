@@ -29,18 +29,9 @@
 namespace sv {
 namespace {
 
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr int kThreads = 256;
-constexpr int kStatsLoads = 4;  // 16-byte loads in flight per thread in rowstats (16 KB chunks)
-constexpr int kResChunk = 8192;  // vocabulary chunk of the residual sums
-constexpr int kResPer = kResChunk / kThreads;  // tokens per thread in a chunk
-constexpr size_t kTsumMaxBytes = size_t(64) << 20;  // cap of the per-thread partial sums
+using namespace acc;  // kThreads, kStatsLoads, kResChunk, kResPer, kCntStride, ReqPlan
 
-struct ReqPlan {
-    int a, n, mode, flag;  // mode 0: residual after a rejection, 1: bonus, 2: nothing to draw
-    int rowP, rowQ;        // target row of P_a (or P_n), draft row of Q_{a+1}
-    float mP, iSP, mQ, iSQ;
-};
+constexpr float kLog2e = 1.4426950408889634f;
 
 struct AcceptArgs {
     const void* target;
@@ -127,9 +118,8 @@ __device__ inline uint32_t arrive(uint32_t* ctr) {
     return __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Arrival counter of request i's draw: alone in a 128-byte cache line, because atomics
-// on one line are serialised and a request's workgroups arrive close together.
-constexpr int kCntStride = 32;  // uint32 per request
+// Arrival counter of request i's draw: alone in a 128-byte cache line (kCntStride), because
+// atomics on one line are serialised and a request's workgroups arrive close together.
 __device__ inline size_t cnt_draw(int i) { return (size_t)i * kCntStride; }
 
 // (max, sum of 2^((x - max) log2e)) of x = l * invT over the chunk [beg, end) of one row,
@@ -890,34 +880,6 @@ __global__ __launch_bounds__(64) void decide_greedy_kernel(AcceptArgs a) {
 
 }  // namespace
 
-AcceptPlan plan_accept(const sv_accept_desc& d) {
-    AcceptPlan p{};
-    const int esz = d.dtype == SV_BF16 ? 2 : 4;
-    const int vec = 16 / esz;
-    p.stats_chunk = kThreads * kStatsLoads * vec;  // 16 KB of logits per workgroup
-    p.stats_chunks = (d.vocab + p.stats_chunk - 1) / p.stats_chunk;
-    p.res_chunk = kResChunk;
-    p.res_chunks = (d.vocab + p.res_chunk - 1) / p.res_chunk;
-    const size_t R = d.num_reqs, b = d.block, D = b > 1 ? b - 1 : 1;
-    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    size_t off = 0;
-    p.off_cnt = off;
-    off = al(off + R * kCntStride * sizeof(uint32_t));
-    p.off_stats_t = off;
-    off = al(off + R * b * p.stats_chunks * sizeof(float2));
-    p.off_stats_q = off;
-    off = al(off + R * D * p.stats_chunks * sizeof(float2));
-    p.off_plan = off;
-    off = al(off + R * sizeof(ReqPlan));
-    p.off_csum = off;
-    off = al(off + R * p.res_chunks * 2 * sizeof(uint64_t));
-    const size_t tsum_bytes = R * p.res_chunks * kThreads * sizeof(uint64_t);
-    p.off_tsum = tsum_bytes <= kTsumMaxBytes ? off : 0;
-    if (p.off_tsum) off = al(off + tsum_bytes);
-    p.total = off;
-    return p;
-}
-
 hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const void* target,
                          const void* draft, const float* draft_stats, const int32_t* draft_tokens,
                          const int32_t* qo_indptr, const float* u_accept, const float* u_sample,
@@ -979,13 +941,6 @@ hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& p, const voi
     hipLaunchKernelGGL((chunksum_kernel<false, float>), gres, dim3(kThreads), 0, stream, a);
     hipLaunchKernelGGL((search_kernel<false, float>), dim3(d.num_reqs), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
-}
-
-size_t draft_stats_workspace(const sv_draft_stats_desc& d) {
-    const int esz = d.dtype == SV_BF16 ? 2 : 4;
-    const int chunk = kThreads * kStatsLoads * (16 / esz);
-    const size_t nc = ((size_t)d.vocab + chunk - 1) / chunk;
-    return (size_t)d.num_reqs * d.drafts * nc * sizeof(float2);
 }
 
 hipError_t launch_draft_stats(const sv_draft_stats_desc& d, const void* logits, float* stats, float* conf, void* ws,

@@ -869,56 +869,6 @@ int ilog2(int x) {
 
 }  // namespace
 
-AttnPlan plan_attn(const sv_attn_desc& d) {
-    AttnPlan p{};
-    const int maxM = (d.num_q_heads / d.num_kv_heads) * d.block;
-    // 8 waves. Up to 128 query rows per kv-head group: a wave owns (32-row group, 32-token
-    // half of each tile), so 64 rows already keep all four SIMDs busy. Above 128 rows a
-    // wave owns 32 rows over the whole tile (256 rows per workgroup), so a group of up to
-    // 256 rows streams its KV once.
-    p.waves = 8;
-    p.halves = maxM > 128 ? 1 : 2;
-    const int rows = (p.waves / p.halves) * 32;
-    p.row_blocks = (maxM + rows - 1) / rows;
-    if (d.dtype == SV_F32) {
-        p.kv_split = 0;
-        p.max_splits = 1;
-        return p;
-    }
-    int split = d.kv_split;
-    if (split <= 0) {
-        // About 8 work items per compute unit if every request had the longest context:
-        // R * Hkv * max_kv_len head-tokens over 256 CUs, divided by 8, at least 2048
-        // tokens. Measured over split sizes 1024..24576, this picks the best or nearly the
-        // best one on c64_b16 (8192), long_c32 (8192), the C5 c64 sweep (16384) and the
-        // small rounds (2048 at 4..16 requests): fewer, longer items save per-item
-        // prologues and merge work until the last items to finish start to dominate, and
-        // below 2048 tokens the per-item costs outweigh the extra parallelism. The host
-        // does not see the lengths themselves (they live on the device), so the bound
-        // uses max_kv_len.
-        long long want = (long long)d.num_reqs * d.num_kv_heads * d.max_kv_len / (256 * 8);
-        if (want < 2048) want = 2048;
-        split = (int)(((want + 63) / 64) * 64);
-    }
-    if (split > d.max_kv_len) split = ((d.max_kv_len + 63) / 64) * 64;
-    // a split's page ids are staged in LDS: at most 1024 pages per split (a split of
-    // n tokens starting on a 64-token boundary touches at most n / P + 2 pages)
-    const long long max_split = 1022LL * d.page_size;
-    if (split > max_split) split = (int)(max_split / 64 * 64);
-    if (split < 64) split = 64;
-    p.kv_split = split;
-    p.max_splits = (d.max_kv_len + split - 1) / split;
-    if (p.max_splits < 1) p.max_splits = 1;
-    if (p.max_splits > 1) {
-        p.part_o_bytes = (size_t)p.max_splits * d.total_q_max * d.num_q_heads * d.head_dim * sizeof(float);
-        p.part_lse_bytes = (size_t)p.max_splits * d.total_q_max * d.num_q_heads * sizeof(float);
-    }
-    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    p.off_groups = al(p.part_o_bytes + p.part_lse_bytes);
-    p.off_ctr = al(p.off_groups + (size_t)d.num_reqs * p.max_splits * sizeof(int32_t));
-    p.ws_bytes = p.off_ctr + 2 * sizeof(int32_t);
-    return p;
-}
 
 hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* q,
                        const void* k_cache, const void* v_cache, const int32_t* page_table,
