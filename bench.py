@@ -35,7 +35,7 @@ ATTN_SRC = os.path.join(ROOT, "paper_2607_25852_amd", "csrc", "attn.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sv_verify_attn_c64_b16_traffic.md")
 COPY_BYTES = 1 << 30  # copy-probe size: 1 GiB read + 1 GiB written, well above the 256 MB MALL
 ATTN_KERNELS = ("attn_plan_kernel", "attn_bf16_kernel", "attn_merge_kernel")
-ACCEPT_KERNELS = ("rowstats_kernel", "chunksum_kernel", "search_kernel")
+ACCEPT_KERNELS = ("rowstats_kernel", "draw_kernel", "chunksum_kernel", "search_kernel")
 # per call kind: its kernels, the kernel dispatched once per call, where the bench records
 # the call's algorithmic bytes
 TRAFFIC_CALLS = {
