@@ -153,13 +153,15 @@ def test_c64_b16_every_unit_on_budget_packing(dev, orc):
 
 def test_long_c32_whole_requests(dev, orc):
     """Long context (64K-128K keys, group 16): every (row, head) of eight whole requests,
-    among them the shortest and longest context and the smallest and largest block."""
+    among them the shortest and longest context, the smallest and largest block, and
+    blocks of 9-10 and 11-12 rows (144..192 query rows per kv-head group)."""
     from paper_2607_25852_amd import synth
     cfg = synth.CONFIGS["long_c32"]
     L = synth.kv_context_lengths(cfg)
     qo = budget_packing("long_c32")
     k = np.diff(qo)
     pick = {int(np.argmin(L)), int(np.argmax(L)), int(np.argmin(k)), int(np.argmax(k))}
+    pick |= {int(np.flatnonzero((k >= 9) & (k <= 10))[0]), int(np.flatnonzero((k >= 11) & (k <= 12))[0])}
     for i in np.random.default_rng(5).permutation(cfg.R):
         if len(pick) == 8:
             break
