@@ -449,35 +449,35 @@ def cpu_round(cfg, rnd, target_s, threads_all):
 def time_round(torch, rnds, steps, stream):
     """Wall-clock time per step over `steps` whole rounds (input copies in turn) with nothing
     else on the stream; then the same steps again with HIP events around each call.
-    Returns (ms per step, {call: mean ms})."""
+    Returns (ms per step, {call: mean ms}); the calls are the round's own (DeviceRound.calls:
+    prepare, attention, acceptance, or budget, pack, attention, acceptance)."""
     import numpy as np
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(steps):
-        r = rnds[s % len(rnds)]
-        r.run_budget()
-        r.run_pack()
-        r.run_attn()
-        r.run_accept()
+        rnds[s % len(rnds)].run()
     torch.cuda.synchronize()
     ms = (time.perf_counter() - t0) * 1e3 / steps
-    calls = ("budget", "pack", "attention", "acceptance")
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(steps)]
+    names = [c for c, _ in rnds[0].calls()]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(steps)]
     torch.cuda.synchronize()
     for s in range(steps):
         e, r = ev[s], rnds[s % len(rnds)]
         e[0].record(stream)
-        r.run_budget()
-        e[1].record(stream)
-        r.run_pack()
-        e[2].record(stream)
-        r.run_attn()
-        e[3].record(stream)
-        r.run_accept()
-        e[4].record(stream)
+        for j, (_, fn) in enumerate(r.calls()):
+            fn()
+            e[j + 1].record(stream)
     torch.cuda.synchronize()
-    per = {c: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j, c in enumerate(calls)}
+    per = {c: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j, c in enumerate(names)}
     return ms, per
+
+
+def call_figures(per):
+    """The per-call times of time_round as the JSON line's `kernels` entries (us)."""
+    out = {f"{c}_us": v * 1e3 for c, v in per.items()}
+    for c in ("prepare", "budget", "pack"):
+        out.setdefault(f"{c}_us", None)
+    return out
 
 
 def copies_for(cfg, L, k, floor_bytes=768 << 20, lo=3, hi=16):
@@ -559,19 +559,18 @@ def main():
     committed = int(np.sum(rnd.accept_len.cpu().numpy() + 1))
     n_warm = warm(torch, step, args.warmup, WARM_SECONDS)
 
-    # the timed steps: the four calls of a round back to back, nothing else on the stream
-    # (HIP events between the calls would add about 10 us per step of their own); then the
-    # same steps with events around each call
+    # the timed steps: the calls of a round back to back, nothing else on the stream (HIP
+    # events between the calls would add about 10 us per step of their own); then the same
+    # steps with events around each call
     ms_step, per = time_round(torch, rnds, args.steps, stream)
-    t_budget, t_pack, t_attn, t_acc = per["budget"], per["pack"], per["attention"], per["acceptance"]
+    t_attn, t_acc = per["attention"], per["acceptance"]
     value = drafts / (ms_step * 1e-3)
     a_bytes = attn_bytes(cfg, rnd.L, k)
     x_bytes = accept_bytes(cfg, k)
     a_gbs = a_bytes / (t_attn * 1e-3) / 1e9
     x_gbs = x_bytes / (t_acc * 1e-3) / 1e9
-    log(f"step {ms_step:.3f} ms: budget {'given depths' if rnd.mode == 'given' else f'{t_budget * 1e3:.1f} us'}, "
-        f"pack {t_pack * 1e3:.1f} us, attention {t_attn * 1e3:.1f} us ({a_gbs:.0f} GB/s), "
-        f"acceptance {t_acc * 1e3:.1f} us ({x_gbs:.0f} GB/s)")
+    log(f"step {ms_step:.3f} ms: " + ", ".join(f"{c} {v * 1e3:.1f} us" for c, v in per.items())
+        + f" (attention {a_gbs:.0f} GB/s, acceptance {x_gbs:.0f} GB/s)")
 
     def post_step_figures():
         """Figures of the calls outside the step, on the same round (first input copy)."""
@@ -608,6 +607,10 @@ def main():
             binding.append_kv(apdesc, k_new, v_new, rnd.page_table, rnd.qo, rnd.ctx_lens, rnd.k_cache, rnd.v_cache)
 
         t_pack_alone = time_loop(torch, stream, rnd.run_pack, args.steps)
+        # the round's set-up and attention as separate calls (sv_alloc_budget alone;
+        # sv_verify_attn building its own work plan), for comparison with the fused step
+        t_budget_alone = time_loop(torch, stream, rnd.run_budget, args.steps) if rnd.mode != "given" else None
+        t_attn_full = time_loop(torch, stream, rnd.run_attn, args.steps)
         t_append = time_loop(torch, stream, append, args.steps)
         ap_bytes = 4.0 * rnd.K * cfg.Hkv * cfg.d * e_sz
 
@@ -683,6 +686,8 @@ def main():
                 "greedy_acceptance_gbs": g_bytes / (t_greedy * 1e-3) / 1e9,
                 "greedy_acceptance_algorithmic_bytes": g_bytes,
                 "pack_alone_us": t_pack_alone * 1e3, "append_us": t_append * 1e3,
+                "budget_alone_us": None if t_budget_alone is None else t_budget_alone * 1e3,
+                "attention_with_own_plan_us": t_attn_full * 1e3,
                 "append_gbs": ap_bytes / (t_append * 1e-3) / 1e9, "append_algorithmic_bytes": ap_bytes,
                 "draft_stats_us": t_dstats * 1e3, "draft_stats_gbs": ds_bytes / (t_dstats * 1e-3) / 1e9,
                 "draft_stats_algorithmic_bytes": ds_bytes,
@@ -742,10 +747,8 @@ def main():
         fig = {"workload": workload_text(c2), "concurrency": c2.R, "block": c2.b, "verified_positions": int(r0.K),
                "verified_drafts": d2, "budget_ratio_index": None if r0.mode == "given" else int(r0.sel[1].item()),
                "input_copies": n_copies, "step_us": ms2 * 1e3, "verified_drafts_per_s": d2 / (ms2 * 1e-3),
-               "budget_us": None if r0.mode == "given" else per2["budget"] * 1e3, "pack_us": per2["pack"] * 1e3,
-               "attention_us": per2["attention"] * 1e3,
+               **call_figures(per2),
                "attention_frac": ab2 / (per2["attention"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
-               "acceptance_us": per2["acceptance"] * 1e3,
                "acceptance_frac": xb2 / (per2["acceptance"] * 1e-3) / 1e9 / HBM_PEAK_GBS,
                "attention_algorithmic_bytes": ab2, "acceptance_algorithmic_bytes": xb2}
         ranges[name] = fig
@@ -780,14 +783,16 @@ def main():
                    "budget_ratio_index": None if rnd.mode == "given" else int(rnd.sel[1].item()),
                    "input_copies": max(1, args.rotate), "input_bytes": main_round_bytes,
                    "parallelism": "single GPU"},
-        "roofline": {"bound": "hbm", "kernel": "sv_verify_attn (plan + split-KV attention + partial merge)",
+        "roofline": {"bound": "hbm",
+                     "kernel": ("sv_verify_attn_run (split-KV attention + partial merge; the work plan is built "
+                                "once per round by sv_prepare_round)" if rnd.fused and rnd.mode != "given" else
+                                "sv_verify_attn (plan + split-KV attention + partial merge)"),
                      "achieved": a_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": a_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "traffic_unit": "HBM bytes per call", "algorithmic_bytes": a_bytes,
                      "call_us": t_attn * 1e3, "attn_source_sha256": attn_source_digest(),
                      "measured_read_peak": read_gbs,
                      "frac_of_measured_read_peak": a_gbs / read_gbs if read_gbs else None},
-        "kernels": {"budget_us": None if rnd.mode == "given" else t_budget * 1e3, "pack_us": t_pack * 1e3,
-                    "attention_us": t_attn * 1e3, "acceptance_us": t_acc * 1e3,
+        "kernels": {**call_figures(per),
                     "acceptance_gbs": x_gbs, "acceptance_frac": x_gbs / HBM_PEAK_GBS,
                     "acceptance_algorithmic_bytes": x_bytes,
                     **extra},

@@ -230,6 +230,46 @@ sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_
                          void* stream);
 size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc);
 
+/*
+ * sv_verify_attn_plan and sv_verify_attn_run -- sv_verify_attn in two parts: the bf16
+ * path's work plan (which (request, kv-head, split, row block) items exist, largest
+ * first) depends only on the descriptor, qo_indptr and kv_lens, so a round builds it once
+ * and every attention layer of that round runs on it, as serving engines plan a batch
+ * once per step (Sec. 4.2: one packed verify batch per round, evaluated by every layer
+ * of the target model).
+ *   sv_verify_attn_plan  writes the plan into ws (sv_verify_attn_workspace_size(desc)
+ *                        bytes); the fp32 path has no plan and the call enqueues nothing.
+ *   sv_verify_attn_run   sv_verify_attn's arguments and results, using the plan that ws
+ *                        holds: it must have been built (by sv_verify_attn_plan or
+ *                        sv_prepare_round) for the same descriptor, qo_indptr and
+ *                        kv_lens. Each run leaves the plan as it found it (its work
+ *                        counter is reset by the last workgroup to finish), so runs on
+ *                        one plan may follow each other on the stream; runs on one
+ *                        workspace must not overlap.
+ * Results equal sv_verify_attn's bit for bit. Errors as for sv_verify_attn.
+ */
+sv_status sv_verify_attn_plan(const sv_attn_desc* desc, const int32_t* qo_indptr, const int32_t* kv_lens,
+                              void* ws, size_t ws_bytes, void* stream);
+sv_status sv_verify_attn_run(const sv_attn_desc* desc, const void* q, const void* k_cache,
+                             const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
+                             const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * sv_prepare_round -- the round's set-up in one launch on one workgroup: sv_alloc_budget
+ * (D-cut, Sec. 4.2), then sv_pack_verify on the budget's own qo_indptr (the packing of
+ * Sec. 4.2), then, when adesc is not NULL, sv_verify_attn_plan over the key counts just
+ * packed, into attn_ws. Arguments and results as in those calls (bdesc and pdesc must
+ * agree on num_reqs and block, as must adesc); the outputs equal theirs bit for bit.
+ * Limits are those of sv_alloc_budget (R <= 4096, R*b <= 8192). Each small call costs a
+ * launch and its gap whatever it does, so the round's three set-up steps share one.
+ */
+sv_status sv_prepare_round(const sv_budget_desc* bdesc, const float* conf, int32_t* keep, int32_t* qo_indptr,
+                           int32_t* sel, float* scores, uint64_t* utility, const sv_pack_desc* pdesc,
+                           const int32_t* block_tokens, const int32_t* ctx_lens, int32_t* tokens,
+                           int32_t* positions, int32_t* kv_lens, const sv_attn_desc* adesc, void* attn_ws,
+                           size_t attn_ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------- */
 /* Speculative acceptance (rejection-sampling verification, Sec. 1; the       */
 /* acceptance probability of eq. mtp-acceptance-tv)                           */

@@ -22,6 +22,7 @@ SV_MAX_RATIOS = 8
 
 # every symbol the header declares (checked by the ABI test)
 EXPORTED = ("sv_alloc_budget", "sv_pack_verify", "sv_append_kv", "sv_verify_attn", "sv_verify_attn_workspace_size",
+            "sv_verify_attn_plan", "sv_verify_attn_run", "sv_prepare_round",
             "sv_spec_accept", "sv_spec_accept_workspace_size", "sv_spec_accept_noalloc", "sv_spec_accept_debug",
             "sv_spec_accept_stats",
             "sv_draft_stats",
@@ -88,6 +89,13 @@ def load() -> ctypes.CDLL:
     lib.sv_alloc_budget.restype = i32
     lib.sv_verify_attn.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
     lib.sv_verify_attn.restype = i32
+    lib.sv_verify_attn_run.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.sv_verify_attn_run.restype = i32
+    lib.sv_verify_attn_plan.argtypes = [ctypes.POINTER(AttnDesc), P, P, P, ctypes.c_size_t, P]
+    lib.sv_verify_attn_plan.restype = i32
+    lib.sv_prepare_round.argtypes = [ctypes.POINTER(BudgetDesc), P, P, P, P, P, P, ctypes.POINTER(PackDesc), P, P, P,
+                                     P, P, ctypes.POINTER(AttnDesc), P, ctypes.c_size_t, P]
+    lib.sv_prepare_round.restype = i32
     lib.sv_verify_attn_workspace_size.argtypes = [ctypes.POINTER(AttnDesc)]
     lib.sv_verify_attn_workspace_size.restype = ctypes.c_size_t
     lib.sv_spec_accept.argtypes = [ctypes.POINTER(AcceptDesc), P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
@@ -209,6 +217,36 @@ def verify_attn(desc: AttnDesc, q, k_cache, v_cache, page_table, qo_indptr, kv_l
     st = load().sv_verify_attn(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
                                _ptr(qo_indptr), _ptr(kv_lens), _ptr(out), _ptr(lse), _ptr(ws), nbytes,
                                _stream(stream))
+    _check(st)
+
+
+def verify_attn_plan(desc: AttnDesc, qo_indptr, kv_lens, ws=None, stream=None):
+    """sv_verify_attn_plan: the work plan of the bf16 path into ws."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().sv_verify_attn_plan(ctypes.byref(desc), _ptr(qo_indptr), _ptr(kv_lens), _ptr(ws), nbytes,
+                                    _stream(stream))
+    _check(st)
+
+
+def verify_attn_run(desc: AttnDesc, q, k_cache, v_cache, page_table, qo_indptr, kv_lens, out, lse=None,
+                    ws=None, stream=None):
+    """sv_verify_attn_run: sv_verify_attn on the plan that ws holds."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
+    st = load().sv_verify_attn_run(ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(page_table),
+                                   _ptr(qo_indptr), _ptr(kv_lens), _ptr(out), _ptr(lse), _ptr(ws), nbytes,
+                                   _stream(stream))
+    _check(st)
+
+
+def prepare_round(bdesc: BudgetDesc, conf, keep, qo_indptr, sel, scores, utility, pdesc, block_tokens, ctx_lens,
+                  tokens, positions, kv_lens, adesc=None, attn_ws=None, stream=None):
+    """sv_prepare_round: budget, packing and (adesc given) the attention work plan in one launch."""
+    nbytes = 0 if attn_ws is None else attn_ws.numel() * attn_ws.element_size()
+    st = load().sv_prepare_round(ctypes.byref(bdesc), _ptr(conf), _ptr(keep), _ptr(qo_indptr), _ptr(sel),
+                                 _ptr(scores), _ptr(utility), ctypes.byref(pdesc), _ptr(block_tokens),
+                                 _ptr(ctx_lens), _ptr(tokens), _ptr(positions), _ptr(kv_lens),
+                                 None if adesc is None else ctypes.byref(adesc), _ptr(attn_ws), nbytes,
+                                 _stream(stream))
     _check(st)
 
 

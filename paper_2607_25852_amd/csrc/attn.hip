@@ -17,6 +17,7 @@
 // interleaved 64-key tiles and merge their softmax states at the end.
 #include <atomic>
 
+#include "attn_plan.h"
 #include "sv_internal.h"
 
 namespace sv {
@@ -31,6 +32,7 @@ typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kTile = 64;  // KV tokens per pipeline step
+static_assert(kTile == kAttnTile, "the work plan counts tiles of the kernel's size");
 
 struct AttnArgs {
     const void* q;
@@ -575,84 +577,18 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     }
 }
 
-// Work list, largest items first. Every (request, split) group is bucketed by its tile
-// count: full splits share the top bucket, a request's shorter last split lands in the
-// bucket of its own length. The buckets are laid out in decreasing size (a counting
-// sort), so the persistent workgroups take the long items early and the short ones fill
-// the tail. The order inside a bucket is unspecified and does not affect any result:
-// every item writes its own output rows or partial slot.
-__device__ inline int plan_splits(const AttnArgs& a, int i, int& last_tiles) {
-    const int q0 = a.qo[i], k_i = a.qo[i + 1] - q0;
-    int kv_len = a.kv_lens[i];
-    if (kv_len > a.max_kv_len) kv_len = a.max_kv_len;
-    last_tiles = 0;
-    if (!(k_i >= 1 && k_i <= a.block && kv_len - k_i >= 0 && q0 >= 0 && q0 + k_i <= a.total_q)) return 0;
-    const int ns = (kv_len + a.split - 1) / a.split;
-    last_tiles = (kv_len - (ns - 1) * a.split + kTile - 1) / kTile;
-    return ns;
-}
-
+// Work list of the persistent kernel (attn_plan.h), built by one workgroup.
 __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnArgs a, int32_t* groups, int32_t* ctr) {
-    constexpr int NB = 1024;  // size buckets (tile counts 1..NB; longer splits share the last)
-    __shared__ int cursor[NB];
-    __shared__ int wsum[16];
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int full_tiles = a.split / kTile;
-    auto bucket = [](int tiles) { return tiles < NB ? tiles - 1 : NB - 1; };
-    const int fb = bucket(full_tiles);
-    cursor[tid] = 0;
-    __syncthreads();
-    // 1. histogram of group sizes (full splits summed per wave first: one shared bucket)
-    for (int base = 0; base < a.R; base += 1024) {
-        const int i = base + tid;
-        int last = 0, ns = i < a.R ? plan_splits(a, i, last) : 0;
-        int full = ns > 1 ? ns - 1 : 0;
-        for (int off = 32; off > 0; off >>= 1) full += __shfl_xor(full, off, 64);
-        if (lane == 0 && full) atomicAdd(&cursor[fb], full);
-        if (ns > 0) atomicAdd(&cursor[bucket(last)], 1);
-    }
-    __syncthreads();
-    // 2. bucket starts in decreasing size: thread t scans bucket NB-1-t
-    const int bk = NB - 1 - tid;
-    const int cnt = cursor[bk];
-    int incl = cnt;
-    for (int off = 1; off < 64; off <<= 1) {
-        const int v = __shfl_up(incl, off, 64);
-        if (lane >= off) incl += v;
-    }
-    if (lane == 63) wsum[w] = incl;
-    __syncthreads();
-    int pre = 0;
-    for (int k = 0; k < w; k++) pre += wsum[k];
-    cursor[bk] = pre + incl - cnt;
-    if (tid == 1023) {
-        ctr[0] = (pre + incl) * a.Hkv * a.nrb;
-        ctr[1] = 0;
-    }
-    __syncthreads();
-    // 3. place the groups (full splits: one atomic per wave, positions by a wave scan)
-    for (int base = 0; base < a.R; base += 1024) {
-        const int i = base + tid;
-        int last = 0, ns = i < a.R ? plan_splits(a, i, last) : 0;
-        const int full = ns > 1 ? ns - 1 : 0;
-        int fincl = full;
-        for (int off = 1; off < 64; off <<= 1) {
-            const int v = __shfl_up(fincl, off, 64);
-            if (lane >= off) fincl += v;
-        }
-        int fbase = 0;
-        if (lane == 63 && fincl) fbase = atomicAdd(&cursor[fb], fincl);
-        fbase = __shfl(fbase, 63, 64);
-        const int p0 = fbase + fincl - full;
-        for (int t = 0; t < full; t++) groups[p0 + t] = (int32_t)(((uint32_t)i << 16) | (uint32_t)t);
-        if (ns > 0) groups[atomicAdd(&cursor[bucket(last)], 1)] = (int32_t)(((uint32_t)i << 16) | (uint32_t)(ns - 1));
-    }
+    __shared__ int cursor[kPlanBuckets];
+    __shared__ int wsum[1024 / 64];
+    AttnPlanArgs pa{a.R, a.block, a.total_q, a.max_kv_len, a.split, a.Hkv, a.nrb, groups, ctr};
+    build_attn_plan<1024>(pa, [&](int i, int& q0, int& k_i, int& kv) {
+        q0 = a.qo[i];
+        k_i = a.qo[i + 1] - q0;
+        kv = a.kv_lens[i];
+    }, cursor, wsum);
 }
 
-// Persistent: one workgroup per CU pulls work items from the counter until the list is
-// exhausted (every wave leaves through the same test).
-// WIDE: row blocks of 256 rows; an item with more than 128 rows left uses whole-tile
-// waves, otherwise half-tile waves (all eight busy on up to 128 rows).
 template <int HD, int NW, int NBUF, bool ONEPAGE, bool WIDE>
 __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const int32_t* __restrict__ groups,
                                                                int32_t* __restrict__ ctr) {
@@ -674,6 +610,13 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
             attn_item<HD, NW, NBUF, ONEPAGE, 1>(a, lds, i, h, s, row0);
         else
             attn_item<HD, NW, NBUF, ONEPAGE, 2>(a, lds, i, h, s, row0);
+    }
+    // the last workgroup to finish leaves the counters as the plan left them, so the
+    // next call on the same plan (another layer of the round) starts clean: every
+    // workgroup has made its last claim before it counts itself here
+    if (threadIdx.x == 0 && atomicAdd(&ctr[2], 1) == (int)gridDim.x - 1) {
+        ctr[1] = 0;
+        ctr[2] = 0;
     }
 }
 
@@ -873,7 +816,7 @@ int ilog2(int x) {
 hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* q,
                        const void* k_cache, const void* v_cache, const int32_t* page_table,
                        const int32_t* qo_indptr, const int32_t* kv_lens, void* out, float* lse,
-                       void* ws, hipStream_t stream) {
+                       void* ws, hipStream_t stream, int phases) {
     AttnArgs a{};
     a.q = q;
     a.kc = k_cache;
@@ -900,7 +843,8 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
     a.scale = d.sm_scale > 0.0f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
     a.scale_log2 = a.scale * kLog2e;
 
-    if (d.dtype == SV_F32) {
+    if (d.dtype == SV_F32) {  // no work plan: one workgroup per (row, head)
+        if (!(phases & kAttnRun)) return hipSuccess;
         const int units = d.total_q_max * d.num_q_heads;
         hipLaunchKernelGGL(attn_f32_kernel, dim3(units), dim3(256), 0, stream, a, d.head_dim);
         return hipGetLastError();
@@ -923,7 +867,8 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
     char* wsb = (char*)ws;
     int32_t* groups = (int32_t*)(wsb + plan.off_groups);
     int32_t* ctr = (int32_t*)(wsb + plan.off_ctr);
-    hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, stream, a, groups, ctr);
+    if (phases & kAttnPlan) hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, stream, a, groups, ctr);
+    if (!(phases & kAttnRun)) return hipGetLastError();
     const dim3 grid(ncu);
 #define SV_LAUNCH_ATTN(HDV, ONEP, HALV) \
     hipLaunchKernelGGL((attn_bf16_kernel<HDV, 8, 4, ONEP, HALV == 1>), grid, dim3(8 * 64), 0, stream, a, groups, ctr)

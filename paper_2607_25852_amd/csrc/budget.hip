@@ -7,6 +7,7 @@
 // registers; only strides of 64 threads or more go through LDS); the top K_j of every
 // candidate ratio are then prefixes of the sorted order, so one prefix sum gives every
 // utility, and the keep counts need no second selection.
+#include "attn_plan.h"
 #include "sv_internal.h"
 
 #pragma clang fp contract(off)
@@ -22,6 +23,21 @@ struct BudgetArgs {
     int R, b, mode, fixed_K, nratios;
     int Kr[SV_MAX_RATIOS];      // K_j per ratio (computed on the host from the descriptor)
     uint32_t cost[SV_MAX_RATIOS];
+};
+
+// The rest of the round's set-up, run by the same workgroup after the budget
+// (sv_prepare_round): the dense verify batch of the kept prefixes (sv_pack_verify's
+// arithmetic) and, when `plan` is set, the verify-attention work plan over the key counts
+// the packing produced (attn_plan.h).
+struct PrepArgs {
+    const int32_t* block_tokens;  // [R, b]
+    const int32_t* ctx;           // [R]
+    int32_t* tokens;              // [total_max]
+    int32_t* positions;           // [total_max]
+    int32_t* kv_lens;             // [R]
+    int total_max;
+    int plan;
+    AttnPlanArgs pa;
 };
 
 __device__ inline float clamp_conf(float c) {
@@ -57,13 +73,13 @@ __device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
 // KPT keys per thread: thread t owns sorted positions t*KPT .. t*KPT+KPT-1. Bitonic
 // stages with stride < KPT run in registers, < 64*KPT across lanes of a wave, the
 // rest through LDS (ping-pong buffers, one barrier per stage).
-template <int KPT>
+template <int KPT, bool PREP>
 __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const float* __restrict__ conf,
                                                           int32_t* __restrict__ keep,
                                                           int32_t* __restrict__ qo_indptr,
                                                           int32_t* __restrict__ sel,
                                                           float* __restrict__ scores_out,
-                                                          uint64_t* __restrict__ util_out) {
+                                                          uint64_t* __restrict__ util_out, PrepArgs pr) {
     constexpr int NPAD = KPT * kThreads;
     __shared__ uint64_t lds[2][NPAD];
     __shared__ int cnt[kMaxReqs];
@@ -201,22 +217,67 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
     __syncthreads();
     int pos = iscan - rsum;
     for (int w = 0; w < wave; w++) pos += scan_tmp[w];
+    // (with PREP the packing offsets also go to LDS, in the key buffers the sort is done with)
+    int* qs = (int*)&lds[0][0];
     for (int e = 0; e < kPer; e++) {
         const int i = tid * kPer + e;
         if (i < R) {
             keep[i] = loc[e] - 1;
             qo_indptr[i] = pos;
+            if (PREP) qs[i] = pos;
         }
         pos += loc[e];
     }
-    if (tid == kThreads - 1) qo_indptr[R] = pos;  // == K
+    if (tid == kThreads - 1) {
+        qo_indptr[R] = pos;  // == K
+        if (PREP) qs[R] = pos;
+    }
+    if constexpr (PREP) {
+        __syncthreads();
+        // 7. the verify batch (sv_pack_verify): row qo[i] + j carries block token j of request
+        //    i at position L_i + j, and kv_lens[i] = L_i + k_i; every load is issued first
+        int tk[KPT], Lc[KPT];
+#pragma unroll
+        for (int e = 0; e < KPT; e++) {
+            const int p = tid + e * kThreads;
+            tk[e] = p < N ? pr.block_tokens[p] : 0;
+            Lc[e] = p < N ? pr.ctx[p / b] : 0;
+        }
+        int* kvs = cnt;  // key counts for the plan (the counts are no longer needed)
+#pragma unroll
+        for (int e = 0; e < KPT; e++) {
+            const int p = tid + e * kThreads;
+            if (p >= N) continue;
+            const int i = p / b, j = p - i * b;
+            const int q0 = qs[i], k_i = qs[i + 1] - q0;
+            const int L = Lc[e];
+            const bool ok = k_i >= 1 && k_i <= b && q0 >= 0 && q0 + k_i <= pr.total_max;
+            if (j == 0) {
+                pr.kv_lens[i] = ok ? L + k_i : L;
+                kvs[i] = ok ? L + k_i : L;
+            }
+            if (ok && j < k_i) {
+                pr.tokens[q0 + j] = tk[e];
+                pr.positions[q0 + j] = L + j;
+            }
+        }
+        if (!pr.plan) return;
+        __syncthreads();
+        // 8. the verify-attention work plan over those key counts
+        int* cursor = qs + ((R + 1 + 63) & ~63);
+        build_attn_plan<kThreads>(pr.pa, [&](int i, int& q0, int& k_i, int& kv) {
+            q0 = qs[i];
+            k_i = qs[i + 1] - q0;
+            kv = kvs[i];
+        }, cursor, scan_tmp);
+    }
 }
 
 }  // namespace
 
-hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* keep,
-                         int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
-                         hipStream_t stream) {
+namespace {
+
+BudgetArgs budget_args(const sv_budget_desc& d) {
     BudgetArgs a{};
     a.R = d.num_reqs;
     a.b = d.block;
@@ -232,9 +293,18 @@ hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* ke
         a.Kr[j] = (int)Kj;
         a.cost[j] = d.cost[j];
     }
-    const int64_t kpt = (N + kThreads - 1) / kThreads;
+    return a;
+}
+
+template <bool PREP>
+hipError_t launch_budget_kernel(const sv_budget_desc& d, const float* conf, int32_t* keep, int32_t* qo_indptr,
+                                int32_t* sel, float* scores, uint64_t* utility, const PrepArgs& pr,
+                                hipStream_t stream) {
+    const BudgetArgs a = budget_args(d);
+    const int64_t kpt = ((int64_t)d.num_reqs * d.block + kThreads - 1) / kThreads;
 #define SV_LAUNCH_BUDGET(KP) \
-    hipLaunchKernelGGL(budget_kernel<KP>, dim3(1), dim3(kThreads), 0, stream, a, conf, keep, qo_indptr, sel, scores, utility)
+    hipLaunchKernelGGL((budget_kernel<KP, PREP>), dim3(1), dim3(kThreads), 0, stream, a, conf, keep, qo_indptr, sel, \
+                       scores, utility, pr)
     if (kpt <= 1) SV_LAUNCH_BUDGET(1);
     else if (kpt <= 2) SV_LAUNCH_BUDGET(2);
     else if (kpt <= 4) SV_LAUNCH_BUDGET(4);
@@ -242,6 +312,35 @@ hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* ke
     else SV_LAUNCH_BUDGET(16);
 #undef SV_LAUNCH_BUDGET
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* keep,
+                         int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
+                         hipStream_t stream) {
+    return launch_budget_kernel<false>(d, conf, keep, qo_indptr, sel, scores, utility, PrepArgs{}, stream);
+}
+
+hipError_t launch_prepare(const sv_budget_desc& d, const float* conf, int32_t* keep, int32_t* qo_indptr,
+                          int32_t* sel, float* scores, uint64_t* utility, const int32_t* block_tokens,
+                          const int32_t* ctx_lens, int32_t* tokens, int32_t* positions, int32_t* kv_lens,
+                          int total_max, const sv_attn_desc* ad, void* attn_ws, hipStream_t stream) {
+    PrepArgs pr{};
+    pr.block_tokens = block_tokens;
+    pr.ctx = ctx_lens;
+    pr.tokens = tokens;
+    pr.positions = positions;
+    pr.kv_lens = kv_lens;
+    pr.total_max = total_max;
+    if (ad && ad->dtype == SV_BF16) {  // the fp32 path has no work plan
+        const AttnPlan p = plan_attn(*ad);
+        pr.plan = 1;
+        pr.pa = AttnPlanArgs{ad->num_reqs, ad->block, ad->total_q_max, ad->max_kv_len, p.kv_split, ad->num_kv_heads,
+                             p.row_blocks, (int32_t*)((char*)attn_ws + p.off_groups),
+                             (int32_t*)((char*)attn_ws + p.off_ctr)};
+    }
+    return launch_budget_kernel<true>(d, conf, keep, qo_indptr, sel, scores, utility, pr, stream);
 }
 
 }  // namespace sv

@@ -39,6 +39,34 @@ sv_status launched(hipError_t e, const char* what) {
 
 }  // namespace
 
+namespace {
+
+// sv_verify_attn and sv_verify_attn_run: the same checks; `phases` says whether the
+// work plan is built here (kAttnAll) or taken from the workspace (kAttnRun)
+sv_status verify_attn(const char* name, int phases, const sv_attn_desc* desc, const void* q, const void* k_cache,
+                      const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
+                      const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes, void* stream) {
+    sv_status st = sv::check_attn(desc);
+    if (st != SV_OK) return st;
+    if (!q || !k_cache || !v_cache || !page_table || !qo_indptr || !kv_lens || !out)
+        return fail(SV_ERR_INVALID_ARG, "%s: a required pointer is NULL", name);
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) || !aligned(ws, 16) ||
+        !aligned(page_table, 4) || !aligned(qo_indptr, 4) || !aligned(kv_lens, 4) || !aligned(lse, 4))
+        return fail(SV_ERR_INVALID_ARG,
+                    "%s: q, caches, out and ws must be 16-byte aligned, int32/fp32 arrays 4-byte aligned", name);
+    const sv::AttnPlan p = sv::plan_attn(*desc);
+    const size_t need = p.ws_bytes;
+    if (need && (!ws || ws_bytes < need))
+        return fail(SV_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given", name, need,
+                    ws ? ws_bytes : (size_t)0);
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "%s: injected launch failure", name);
+    return launched(sv::launch_attn(*desc, p, q, k_cache, v_cache, page_table, qo_indptr, kv_lens, out, lse, ws,
+                                    (hipStream_t)stream, phases),
+                    name);
+}
+
+}  // namespace
+
 extern "C" {
 
 sv_status sv_alloc_budget(const sv_budget_desc* desc, const float* conf, int32_t* keep,
@@ -57,28 +85,77 @@ size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc) {
     return sv::plan_attn(*desc).ws_bytes;
 }
 
+
 sv_status sv_verify_attn(const sv_attn_desc* desc, const void* q, const void* k_cache,
                          const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
                          const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes,
                          void* stream) {
     CallRange range("sv_verify_attn");
+    return verify_attn("sv_verify_attn", sv::kAttnAll, desc, q, k_cache, v_cache, page_table, qo_indptr, kv_lens, out,
+                       lse, ws, ws_bytes, stream);
+}
+
+sv_status sv_verify_attn_run(const sv_attn_desc* desc, const void* q, const void* k_cache,
+                             const void* v_cache, const int32_t* page_table, const int32_t* qo_indptr,
+                             const int32_t* kv_lens, void* out, float* lse, void* ws, size_t ws_bytes,
+                             void* stream) {
+    CallRange range("sv_verify_attn_run");
+    return verify_attn("sv_verify_attn_run", sv::kAttnRun, desc, q, k_cache, v_cache, page_table, qo_indptr, kv_lens,
+                       out, lse, ws, ws_bytes, stream);
+}
+
+sv_status sv_verify_attn_plan(const sv_attn_desc* desc, const int32_t* qo_indptr, const int32_t* kv_lens, void* ws,
+                              size_t ws_bytes, void* stream) {
+    CallRange range("sv_verify_attn_plan");
     sv_status st = sv::check_attn(desc);
     if (st != SV_OK) return st;
-    if (!q || !k_cache || !v_cache || !page_table || !qo_indptr || !kv_lens || !out)
-        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn: a required pointer is NULL");
-    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(out, 16) || !aligned(ws, 16) ||
-        !aligned(page_table, 4) || !aligned(qo_indptr, 4) || !aligned(kv_lens, 4) || !aligned(lse, 4))
-        return fail(SV_ERR_INVALID_ARG,
-                    "sv_verify_attn: q, caches, out and ws must be 16-byte aligned, int32/fp32 arrays 4-byte aligned");
+    if (!qo_indptr || !kv_lens) return fail(SV_ERR_INVALID_ARG, "sv_verify_attn_plan: a required pointer is NULL");
+    if (!aligned(qo_indptr, 4) || !aligned(kv_lens, 4) || !aligned(ws, 16))
+        return fail(SV_ERR_INVALID_ARG, "sv_verify_attn_plan: int32 arrays 4-byte aligned, ws 16-byte aligned");
     const sv::AttnPlan p = sv::plan_attn(*desc);
-    const size_t need = p.ws_bytes;
-    if (need && (!ws || ws_bytes < need))
-        return fail(SV_ERR_WORKSPACE, "sv_verify_attn: workspace of %zu bytes needed, %zu given", need,
+    if (p.ws_bytes && (!ws || ws_bytes < p.ws_bytes))
+        return fail(SV_ERR_WORKSPACE, "sv_verify_attn_plan: workspace of %zu bytes needed, %zu given", p.ws_bytes,
                     ws ? ws_bytes : (size_t)0);
-    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_verify_attn: injected launch failure");
-    return launched(sv::launch_attn(*desc, p, q, k_cache, v_cache, page_table, qo_indptr, kv_lens, out, lse, ws,
-                                    (hipStream_t)stream),
-                    "sv_verify_attn");
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_verify_attn_plan: injected launch failure");
+    return launched(sv::launch_attn(*desc, p, nullptr, nullptr, nullptr, nullptr, qo_indptr, kv_lens, nullptr, nullptr,
+                                    ws, (hipStream_t)stream, sv::kAttnPlan),
+                    "sv_verify_attn_plan");
+}
+
+sv_status sv_prepare_round(const sv_budget_desc* bdesc, const float* conf, int32_t* keep, int32_t* qo_indptr,
+                           int32_t* sel, float* scores, uint64_t* utility, const sv_pack_desc* pdesc,
+                           const int32_t* block_tokens, const int32_t* ctx_lens, int32_t* tokens, int32_t* positions,
+                           int32_t* kv_lens, const sv_attn_desc* adesc, void* attn_ws, size_t attn_ws_bytes,
+                           void* stream) {
+    CallRange range("sv_prepare_round");
+    sv_status st = sv::check_budget(bdesc, conf, keep, qo_indptr, sel);
+    if (st != SV_OK) return st;
+    if ((st = sv::check_pack(pdesc)) != SV_OK) return st;
+    if (pdesc->num_reqs != bdesc->num_reqs || pdesc->block != bdesc->block)
+        return fail(SV_ERR_INVALID_ARG, "sv_prepare_round: the packing's num_reqs/block (%d, %d) differ from the "
+                                        "budget's (%d, %d)",
+                    pdesc->num_reqs, pdesc->block, bdesc->num_reqs, bdesc->block);
+    if (!block_tokens || !ctx_lens || !tokens || !positions || !kv_lens)
+        return fail(SV_ERR_INVALID_ARG, "sv_prepare_round: a required pointer is NULL");
+    if (!aligned(block_tokens, 4) || !aligned(ctx_lens, 4) || !aligned(tokens, 4) || !aligned(positions, 4) ||
+        !aligned(kv_lens, 4) || !aligned(attn_ws, 16))
+        return fail(SV_ERR_INVALID_ARG, "sv_prepare_round: int32 arrays 4-byte aligned, attn_ws 16-byte aligned");
+    if (adesc) {
+        if ((st = sv::check_attn(adesc)) != SV_OK) return st;
+        if (adesc->num_reqs != bdesc->num_reqs || adesc->block != bdesc->block)
+            return fail(SV_ERR_INVALID_ARG, "sv_prepare_round: the attention's num_reqs/block (%d, %d) differ from "
+                                            "the budget's (%d, %d)",
+                        adesc->num_reqs, adesc->block, bdesc->num_reqs, bdesc->block);
+        const size_t need = sv::plan_attn(*adesc).ws_bytes;
+        if (need && (!attn_ws || attn_ws_bytes < need))
+            return fail(SV_ERR_WORKSPACE, "sv_prepare_round: attention workspace of %zu bytes needed, %zu given",
+                        need, attn_ws ? attn_ws_bytes : (size_t)0);
+    }
+    if (inject_launch_fault()) return fail(SV_ERR_HIP, "sv_prepare_round: injected launch failure");
+    return launched(sv::launch_prepare(*bdesc, conf, keep, qo_indptr, sel, scores, utility, block_tokens, ctx_lens,
+                                       tokens, positions, kv_lens, pdesc->total_max, adesc, attn_ws,
+                                       (hipStream_t)stream),
+                    "sv_prepare_round");
 }
 
 sv_status sv_pack_verify(const sv_pack_desc* desc, const int32_t* block_tokens, const int32_t* ctx_lens,

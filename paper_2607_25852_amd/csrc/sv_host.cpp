@@ -243,7 +243,7 @@ AttnPlan plan_attn(const sv_attn_desc& d) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     p.off_groups = al(p.part_o_bytes + p.part_lse_bytes);
     p.off_ctr = al(p.off_groups + (size_t)d.num_reqs * p.max_splits * sizeof(int32_t));
-    p.ws_bytes = p.off_ctr + 2 * sizeof(int32_t);
+    p.ws_bytes = p.off_ctr + 3 * sizeof(int32_t);  // work items, work counter, finished workgroups
     return p;
 }
 

@@ -35,7 +35,7 @@ struct AttnPlan {
     size_t part_o_bytes;    // split partial outputs (fp32), offset 0
     size_t part_lse_bytes;  // split partial log-sum-exps, after part_o
     size_t off_groups;      // work list of the persistent kernel
-    size_t off_ctr;         // {number of work items, work counter}
+    size_t off_ctr;         // {number of work items, work counter, finished workgroups}
     size_t ws_bytes;        // total workspace (0 for the fp32 path)
 };
 struct AcceptPlan {

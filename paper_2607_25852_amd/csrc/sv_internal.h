@@ -16,12 +16,20 @@ namespace sv {
 hipError_t launch_budget(const sv_budget_desc& d, const float* conf, int32_t* keep,
                          int32_t* qo_indptr, int32_t* sel, float* scores, uint64_t* utility,
                          hipStream_t stream);
+// the budget, the verify batch of the kept prefixes and (ad: bf16 attention) the
+// verify-attention work plan in attn_ws, by one workgroup (sv_prepare_round)
+hipError_t launch_prepare(const sv_budget_desc& d, const float* conf, int32_t* keep, int32_t* qo_indptr,
+                          int32_t* sel, float* scores, uint64_t* utility, const int32_t* block_tokens,
+                          const int32_t* ctx_lens, int32_t* tokens, int32_t* positions, int32_t* kv_lens,
+                          int total_max, const sv_attn_desc* ad, void* attn_ws, hipStream_t stream);
 
 // ---- verify attention -----------------------------------------------------------
+// what launch_attn runs: the work plan, the attention (and the merge of split partials), or both
+enum AttnPhases { kAttnPlan = 1, kAttnRun = 2, kAttnAll = 3 };
 hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* q,
                        const void* k_cache, const void* v_cache, const int32_t* page_table,
                        const int32_t* qo_indptr, const int32_t* kv_lens, void* out, float* lse,
-                       void* ws, hipStream_t stream);
+                       void* ws, hipStream_t stream, int phases = kAttnAll);
 
 // ---- acceptance -----------------------------------------------------------------
 hipError_t launch_accept(const sv_accept_desc& d, const AcceptPlan& plan, const void* target,

@@ -1,12 +1,15 @@
 """One draft-verify round on the GPU through libspecverify.
 
 `DeviceRound` owns the torch device buffers of a round (inputs already resident
-in HBM, outputs, workspaces) and issues the C-ABI calls on one stream:
-sv_alloc_budget -> sv_pack_verify -> sv_verify_attn -> sv_spec_accept. It only moves data and
-marshals arguments; all arithmetic of the round runs in the library's kernels.
+in HBM, outputs, workspaces) and issues the C-ABI calls on one stream. By default
+(`fused`) these are sv_prepare_round -> sv_verify_attn_run -> sv_spec_accept, where
+the first call does the budget, the packing and the attention work plan in one
+launch. Otherwise they are the separate calls sv_alloc_budget -> sv_pack_verify ->
+sv_verify_attn -> sv_spec_accept. It only moves data and marshals arguments; all
+arithmetic of the round runs in the library's kernels.
 
 The round is self-contained on the device: the budget writes qo_indptr, the packing
-call turns it and the committed context lengths into the key counts kv_lens = L_i + k_i
+turns it and the committed context lengths into the key counts kv_lens = L_i + k_i
 that attention reads, and acceptance reads the same qo_indptr. No per-round value
 crosses to the host between the calls.
 """
@@ -43,8 +46,9 @@ class DeviceRound:
 
     def __init__(self, cfg: synth.RoundConfig, kind: str = "logits", with_attn: bool = True,
                  with_accept: bool = True, fill_unused=0.0, device="cuda", kv_split: int = 0,
-                 logits=None, kv=None):
+                 logits=None, kv=None, fused: bool = True):
         self.cfg = cfg
+        self.fused = fused
         self.kind = kind
         self.device = device
         R, b, D = cfg.R, cfg.b, cfg.D
@@ -187,10 +191,36 @@ class DeviceRound:
         B.spec_accept(self.xdesc, self.target, self.draft, self.tokens, self.qo, self.u_accept, self.u_sample,
                       self.accept_len, self.out_tokens, self.flags, self.acc_ws, stream)
 
-    def run(self, stream=None):
-        self.run_budget(stream)
-        self.run_pack(stream)
-        if self.with_attn:
-            self.run_attn(stream)
+    def run_prepare(self, stream=None):
+        """sv_prepare_round: the budget, the packing and the attention work plan, one launch."""
+        B.prepare_round(self.bdesc, self.conf, self.keep, self.qo, self.sel, self.scores, self.util, self.pdesc,
+                        self.block_tokens, self.ctx_lens, self.v_tokens, self.v_positions, self.kv_lens,
+                        self.adesc if self.with_attn else None, self.attn_ws if self.with_attn else None, stream)
+
+    def run_attn_planned(self, stream=None):
+        """sv_verify_attn_run on the plan run_prepare left in the attention workspace."""
+        B.verify_attn_run(self.adesc, self.q, self.k_cache, self.v_cache, self.page_table, self.qo, self.kv_lens,
+                          self.attn_out, self.attn_lse, self.attn_ws, stream)
+
+    def calls(self):
+        """The round's calls in order, as (name, function of stream): with `fused` (and a
+        budget stage) sv_prepare_round, then the attention on its plan; otherwise budget,
+        packing and the attention with its own plan as separate calls."""
+        out = []
+        if self.fused and self.mode != "given":
+            out.append(("prepare", self.run_prepare))
+            if self.with_attn:
+                out.append(("attention", self.run_attn_planned))
+        else:
+            if self.mode != "given":
+                out.append(("budget", self.run_budget))
+            out.append(("pack", self.run_pack))
+            if self.with_attn:
+                out.append(("attention", self.run_attn))
         if self.with_accept:
-            self.run_accept(stream)
+            out.append(("acceptance", self.run_accept))
+        return out
+
+    def run(self, stream=None):
+        for _, fn in self.calls():
+            fn(stream)

@@ -283,3 +283,42 @@ def test_probe_header_declarations_are_exported():
     assert lib.svprobe_stream_read(ctypes.c_void_p(4096), 1000, ctypes.c_void_p(4096), None) == -1
     assert lib.svprobe_stream_read(ctypes.c_void_p(4100), 32768, ctypes.c_void_p(4096), None) == -1
 
+
+
+def test_prepare_round_and_attention_plan_checks(lib, monkeypatch):
+    """sv_prepare_round, sv_verify_attn_plan and sv_verify_attn_run reject bad calls on the
+    host (fake pointers never dereferenced; SV_FAULT_INJECT stops valid calls before any
+    launch)."""
+    fake = ctypes.c_void_p(256)
+    bd = B.budget_desc(4, 8, "fixed", fixed_budget=32)
+    pd = B.pack_desc(4, 8, 32)
+    ad = B.attn_desc(4, 32, 8, 32, 8, 128, 64, 130, 1000, 8200, B.SV_BF16)
+    need = lib.sv_verify_attn_workspace_size(ctypes.byref(ad))
+
+    def prep(bdesc, pdesc, adesc, ws_bytes, ptr=fake):
+        return lib.sv_prepare_round(ctypes.byref(bdesc), fake, fake, fake, fake, None, None, ctypes.byref(pdesc),
+                                    ptr, fake, fake, fake, fake, None if adesc is None else ctypes.byref(adesc),
+                                    fake, ws_bytes, None)
+    # the packing and the attention descriptors must agree with the budget's
+    assert prep(bd, B.pack_desc(5, 8, 32), None, 0) == B.SV_ERR_INVALID_ARG and "packing" in B.last_error()
+    assert prep(bd, B.pack_desc(4, 9, 36), None, 0) == B.SV_ERR_INVALID_ARG and "packing" in B.last_error()
+    bad_a = B.attn_desc(5, 32, 8, 32, 8, 128, 64, 130, 1000, 8200, B.SV_BF16)
+    assert prep(bd, pd, bad_a, need) == B.SV_ERR_INVALID_ARG and "attention" in B.last_error()
+    assert prep(bd, pd, ad, need - 1) == B.SV_ERR_WORKSPACE
+    assert prep(bd, pd, ad, need, ptr=None) == B.SV_ERR_INVALID_ARG and "NULL" in B.last_error()
+    assert prep(B.budget_desc(4, 8, "fixed", fixed_budget=33), pd, None, 0) == B.SV_ERR_INVALID_ARG
+    # plan and run: the attention descriptor's checks, then pointers and workspace
+    assert lib.sv_verify_attn_plan(ctypes.byref(B.attn_desc(4, 32, 8, 32, 3, 128, 64, 130, 1000, 8200,
+                                                            B.SV_BF16)), fake, fake, fake, need,
+                                   None) == B.SV_ERR_INVALID_ARG
+    assert lib.sv_verify_attn_plan(ctypes.byref(ad), None, fake, fake, need, None) == B.SV_ERR_INVALID_ARG
+    assert lib.sv_verify_attn_plan(ctypes.byref(ad), fake, fake, fake, need - 1, None) == B.SV_ERR_WORKSPACE
+    assert lib.sv_verify_attn_run(ctypes.byref(ad), None, None, None, None, None, None, None, None, fake, need,
+                                  None) == B.SV_ERR_INVALID_ARG
+    assert lib.sv_verify_attn_run(ctypes.byref(ad), fake, fake, fake, fake, fake, fake, fake, None, fake, need - 1,
+                                  None) == B.SV_ERR_WORKSPACE
+    monkeypatch.setenv("SV_FAULT_INJECT", "launch")
+    assert prep(bd, pd, ad, need) == B.SV_ERR_HIP and "sv_prepare_round" in B.last_error()
+    assert lib.sv_verify_attn_plan(ctypes.byref(ad), fake, fake, fake, need, None) == B.SV_ERR_HIP
+    assert lib.sv_verify_attn_run(ctypes.byref(ad), fake, fake, fake, fake, fake, fake, fake, None, fake, need,
+                                  None) == B.SV_ERR_HIP
