@@ -510,6 +510,9 @@ def main():
                     help="print HBM traffic per call from two rocprofv3 --pmc runs")
     ap.add_argument("--traffic-call", choices=sorted(TRAFFIC_CALLS), default="attention",
                     help="the call --summarize-traffic reports")
+    ap.add_argument("--unfused", action="store_true",
+                    help="step as separate calls: sv_alloc_budget, sv_pack_verify, sv_verify_attn (its own plan), "
+                         "sv_spec_accept")
     ap.add_argument("--step-only", action="store_true",
                     help="time the steps only: no greedy, packing, draft-statistics, graph, read-probe, other "
                          "workloads or host baseline (for counter runs)")
@@ -536,7 +539,7 @@ def main():
     cfg = synth.CONFIGS[args.workload]
     log("generating inputs", cfg.name)
     t0 = time.perf_counter()
-    rnd = DeviceRound(cfg, kind="logits", kv_split=args.kv_split)
+    rnd = DeviceRound(cfg, kind="logits", kv_split=args.kv_split, fused=not args.unfused)
     rnds = [rnd] + [rnd.replica() for _ in range(max(1, args.rotate) - 1)]
     torch.cuda.synchronize()
     log(f"inputs resident ({time.perf_counter() - t0:.1f} s, {len(rnds)} copies); K={rnd.K}")
@@ -730,7 +733,7 @@ def main():
     for name in names:
         c2 = synth.CONFIGS[name]
         t1 = time.perf_counter()
-        r0 = DeviceRound(c2, kind="logits", kv="device")
+        r0 = DeviceRound(c2, kind="logits", kv="device", fused=not args.unfused)
         k2 = np.diff(r0.qo_host)
         n_copies = copies_for(c2, r0.L, k2)
         rr = [r0] + [r0.replica() for _ in range(n_copies - 1)]
