@@ -245,7 +245,9 @@ size_t sv_verify_attn_workspace_size(const sv_attn_desc* desc);
  *                        kv_lens. Each run leaves the plan as it found it (its work
  *                        counter is reset by the last workgroup to finish), so runs on
  *                        one plan may follow each other on the stream; runs on one
- *                        workspace must not overlap.
+ *                        workspace must not overlap. On a workspace that holds no plan,
+ *                        or a plan built for other inputs, the results are unspecified
+ *                        but every memory access stays in bounds.
  * Results equal sv_verify_attn's bit for bit. Errors as for sv_verify_attn.
  */
 sv_status sv_verify_attn_plan(const sv_attn_desc* desc, const int32_t* qo_indptr, const int32_t* kv_lens,

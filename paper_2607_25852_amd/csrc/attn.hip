@@ -48,6 +48,7 @@ struct AttnArgs {
     int R, total_q, Hq, Hkv, G, block;
     int log2P, maxp, num_pages, max_kv_len;
     int split, max_splits, nrb;  // nrb: row blocks (16 rows per wave) per (request, kv-head)
+    int max_items;               // R * max_splits * Hkv * nrb (capped at INT_MAX): the longest work list
     float scale_log2;  // sm_scale * log2(e)
     float scale;       // sm_scale
 };
@@ -594,17 +595,22 @@ __global__ __launch_bounds__(NW * 64, 1) void attn_bf16_kernel(AttnArgs a, const
                                                                int32_t* __restrict__ ctr) {
     __shared__ __attribute__((aligned(16))) LdsRing<HD, NBUF> lds;
     __shared__ int s_item;
-    const int nitems = ctr[0];
+    // A work list that was never built (a run on a workspace without a plan) holds arbitrary
+    // values: its length is capped by the longest possible list, a negative claim ends the
+    // loop and items naming a request or split that does not exist are skipped, so every
+    // access stays in bounds (the results are then unspecified).
+    const int nitems = min(ctr[0], a.max_items);
     const int per_group = a.Hkv * a.nrb;
     for (;;) {
         if (threadIdx.x == 0) s_item = atomicAdd(&ctr[1], 1);
         __syncthreads();
         const int item = s_item;
         __syncthreads();
-        if (item >= nitems) break;
+        if (item < 0 || item >= nitems) break;
         const uint32_t gv = (uint32_t)groups[item / per_group];  // request << 16 | split
         const int within = item % per_group;
         const int i = (int)(gv >> 16), h = within / a.nrb, s = (int)(gv & 0xFFFFu);
+        if (i >= a.R || s >= a.max_splits) continue;
         const int row0 = (within % a.nrb) * (WIDE ? 2 * NW * 16 : NW * 16);
         if (WIDE && a.G * (a.qo[i + 1] - a.qo[i]) - row0 > NW * 16)
             attn_item<HD, NW, NBUF, ONEPAGE, 1>(a, lds, i, h, s, row0);
@@ -840,6 +846,10 @@ hipError_t launch_attn(const sv_attn_desc& d, const AttnPlan& plan, const void* 
     a.max_kv_len = d.max_kv_len;
     a.split = plan.kv_split;
     a.max_splits = plan.max_splits;
+    {
+        const long long mi = (long long)d.num_reqs * plan.max_splits * d.num_kv_heads * plan.row_blocks;
+        a.max_items = mi > 0x7FFFFFFFLL ? 0x7FFFFFFF : (int)mi;
+    }
     a.scale = d.sm_scale > 0.0f ? d.sm_scale : 1.0f / sqrtf((float)d.head_dim);
     a.scale_log2 = a.scale * kLog2e;
 

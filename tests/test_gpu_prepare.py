@@ -149,3 +149,47 @@ def test_prepare_round_budget_and_packing_edges(dev, orc, R, b, total_cut):
     for got, want in ((f["tokens"].cpu().numpy(), tok), (f["positions"].cpu().numpy(), pos)):
         np.testing.assert_array_equal(got[want >= 0], want[want >= 0])  # the rows written
         assert np.all(got[want < 0] == -7)  # rows no request owns are left alone
+
+
+def test_attention_run_on_a_workspace_without_its_plan(dev):
+    """sv_verify_attn_run on a workspace that holds no plan, or the plan of other inputs:
+    the results are unspecified, but the call must succeed and every access stay in bounds.
+    The workspace is filled with uniform bytes and with the 8-byte pattern (0x7FFFFFFF, 0),
+    which makes the item count the largest int, the work counter 0 and every other work
+    item name request 32767 (beyond the last); then the plan of a round with other key
+    counts is used. A plan built afterwards must give sv_verify_attn's results bit for bit."""
+    import torch
+    from paper_2607_25852_amd import binding as B, synth
+    from paper_2607_25852_amd.round import DeviceRound
+    cfg = synth.CONFIGS["c64_b16"]
+    say("attention run without its plan", cfg.name)
+    rnd = DeviceRound(cfg, kind="logits", fused=False, with_accept=False)
+    rnd.run_attn()
+    torch.cuda.synchronize()
+    K = rnd.K
+    ref_out, ref_lse = rnd.attn_out[:K].clone(), rnd.attn_lse[:K].clone()
+    ws32 = rnd.attn_ws.view(torch.int32)
+    fills = [("byte", v) for v in (0x00, 0x01, 0x7F, 0xFF)] + [("pattern", None)]
+    for kind, v in fills:
+        if kind == "byte":
+            rnd.attn_ws.fill_(v)
+        else:
+            ws32[0::2] = 0x7FFFFFFF
+            ws32[1::2] = 0
+        rnd.run_attn_planned()
+        torch.cuda.synchronize()
+    # the plan of other inputs: every request's context halved
+    qo = rnd.qo.cpu().numpy()
+    kv_a = rnd.kv_lens.cpu().numpy()
+    k = np.diff(qo)
+    kv_b = torch.from_numpy((kv_a - (kv_a - k) // 2).astype(np.int32)).cuda()
+    B.verify_attn_plan(rnd.adesc, rnd.qo, kv_b, rnd.attn_ws)
+    rnd.run_attn_planned()
+    torch.cuda.synchronize()
+    # and back: a plan for these inputs restores the exact results
+    rnd.attn_out.fill_(-3.0)
+    B.verify_attn_plan(rnd.adesc, rnd.qo, rnd.kv_lens, rnd.attn_ws)
+    rnd.run_attn_planned()
+    torch.cuda.synchronize()
+    assert torch.equal(rnd.attn_out[:K], ref_out)
+    assert torch.equal(rnd.attn_lse[:K], ref_lse)
