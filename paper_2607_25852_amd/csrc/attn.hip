@@ -171,6 +171,25 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
     const int limit = L + jq;  // last visible key of this row (inclusive)
     const int last_key = min(limit, tok_end - 1);  // ... and of this split
 
+    // Per-lane element offsets of the V^T transpose reads inside a tile's V buffer: read
+    // (qh, d-tile t) of 16-token k-chunk c lies at 16c*HD + vofs[qh][t] (for half-tile waves
+    // c counts from their own half, whose offset vofs includes). The swizzle sees only the
+    // token's position mod 16, which c does not change, so these 2*DT values serve every
+    // chunk of every tile and each read costs one add of the buffer base.
+    int vofs[2][DT];
+    {
+        const int g = lane >> 4, jl = lane & 15;
+#pragma unroll
+        for (int qh = 0; qh < 2; qh++) {
+            const int tl = 8 * qh + 4 * (g >> 1) + (jl >> 2);  // token mod 16
+#pragma unroll
+            for (int t = 0; t < DT; t++) {
+                const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
+                vofs[qh][t] = (HALVES == 2 ? th * 32 * HD : 0) + tl * HD +
+                              (((dd >> 3) ^ (swz(tl) & (CPR - 1))) << 3) + (dd & 7);
+            }
+        }
+    }
     const uint16_t* __restrict__ qp = (const uint16_t*)a.q;
     const uint16_t* __restrict__ kcp = (const uint16_t*)a.kc;
     const uint16_t* __restrict__ vcp = (const uint16_t*)a.vc;
@@ -349,15 +368,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
             constexpr int NT = NSB * NJ;  // PV MFMAs per tile for this wave
             constexpr int VPD = 4;
             auto vread = [&](int J) {
-                const int hh = HALVES == 2 ? th : J / NJ;
-                const int c = 2 * hh + (J % NJ) / DT, t = J % DT;
+                const int c = 2 * (J / NJ) + (J % NJ) / DT, t = J % DT;  // (whole-tile waves)
                 i16x4 vq[2];
     #pragma unroll
                 for (int qh = 0; qh < 2; qh++) {
-                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
-                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
-                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
-                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                    const uint16_t* addr = vt + 16 * c * HD + vofs[qh][t];
                     vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
                 }
                 return __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
@@ -440,14 +455,11 @@ __device__ __forceinline__ void attn_item(const AttnArgs& a, LdsRing<HD, NBUF>& 
             constexpr int NJ = 2 * DT;
             constexpr int VPD = 4;
             auto vread = [&](int j) {
-                const int c = 2 * hh + j / DT, t = j % DT;
+                const int c = j / DT, t = j % DT;  // chunk within the wave's half
                 i16x4 vq[2];
 #pragma unroll
                 for (int qh = 0; qh < 2; qh++) {
-                    const int tok = 16 * c + 8 * qh + 4 * (g >> 1) + (jl >> 2);
-                    const int dd = 32 * t + 16 * (g & 1) + 4 * (jl & 3);
-                    const int pos = ((dd >> 3) ^ (swz(tok) & (CPR - 1)));
-                    const uint16_t* addr = vt + tok * HD + pos * 8 + (dd & 7);
+                    const uint16_t* addr = vt + 16 * c * HD + vofs[qh][t];
                     vq[qh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)addr);
                 }
                 return __builtin_shufflevector(vq[0], vq[1], 0, 1, 2, 3, 4, 5, 6, 7);
