@@ -15,7 +15,9 @@
 namespace sv {
 namespace {
 
-constexpr int kThreads = 512;
+constexpr int kThreads = 512;  // the workgroup of large rounds
+constexpr int kWave = 64;      // the workgroup of small rounds: one wave
+constexpr int kSmallMax = 128; // small rounds: R*b <= 128 (up to two keys per lane)
 constexpr int kMaxKeys = SV_MAX_BUDGET_POSITIONS;
 constexpr int kMaxReqs = SV_MAX_BUDGET_REQS;
 
@@ -70,23 +72,30 @@ __device__ inline uint64_t shfl_up_u64(uint64_t v, int d) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-// KPT keys per thread: thread t owns sorted positions t*KPT .. t*KPT+KPT-1. Bitonic
-// stages with stride < KPT run in registers, < 64*KPT across lanes of a wave, the
-// rest through LDS (ping-pong buffers, one barrier per stage).
-template <int KPT, bool PREP>
-__global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const float* __restrict__ conf,
+// NT threads, KPT keys per thread: thread t owns sorted positions t*KPT .. t*KPT+KPT-1.
+// Bitonic stages with stride < KPT run in registers, < 64*KPT across lanes of a wave, the
+// rest through LDS (ping-pong buffers, one barrier per stage). Small rounds run on one
+// wave (NT = 64, at most 128 keys), where every stage stays in registers and shuffles
+// and the barriers are a single wave's. (At 256 keys the one-wave form's sort is still
+// faster, but its attention plan, 1024 buckets over 64 threads, costs more than that.)
+template <int NT, int KPT, bool PREP>
+__global__ __launch_bounds__(NT) void budget_kernel(BudgetArgs a, const float* __restrict__ conf,
                                                           int32_t* __restrict__ keep,
                                                           int32_t* __restrict__ qo_indptr,
                                                           int32_t* __restrict__ sel,
                                                           float* __restrict__ scores_out,
                                                           uint64_t* __restrict__ util_out, PrepArgs pr) {
-    constexpr int NPAD = KPT * kThreads;
+    static_assert(NT == kThreads || (NT == kWave && KPT * NT <= kSmallMax), "budget workgroup");
+    constexpr int NPAD = KPT * NT;
+    // requests: up to kMaxReqs (large rounds) or kSmallMax (one wave); with PREP the
+    // one-wave form keeps the attention plan's bucket cursors after them
+    constexpr int NCNT = NT == kThreads ? kMaxReqs : kSmallMax + kPlanBuckets;
     __shared__ uint64_t lds[2][NPAD];
-    __shared__ int cnt[kMaxReqs];
-    __shared__ uint64_t wtot[kThreads / 64];
+    __shared__ int cnt[NCNT];
+    __shared__ uint64_t wtot[NT / 64];
     __shared__ uint64_t s_util[SV_MAX_RATIOS];
     __shared__ int s_K;
-    __shared__ int scan_tmp[kThreads / 64];
+    __shared__ int scan_tmp[NT / 64];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int R = a.R, b = a.b, N = R * b;
@@ -95,9 +104,9 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
     //    the confidences are first staged through LDS with coalesced loads (buffer 1 of
     //    the key storage is free until the first LDS stage of the sort)
     float* cst = (float*)&lds[1][0];
-    for (int e = tid; e < R * (b - 1); e += kThreads) cst[e] = conf[e];
+    for (int e = tid; e < R * (b - 1); e += NT) cst[e] = conf[e];
     __syncthreads();
-    for (int i = tid; i < R; i += kThreads) {
+    for (int i = tid; i < R; i += NT) {
         float s = 1.0f;
         for (int t = 0; t < b; t++) {
             if (t > 0) s = s * clamp_conf(cst[i * (b - 1) + (t - 1)]);
@@ -107,7 +116,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
         }
         cnt[i] = 0;
     }
-    for (int p = N + tid; p < NPAD; p += kThreads) lds[0][p] = 0;  // below every real key
+    for (int p = N + tid; p < NPAD; p += NT) lds[0][p] = 0;  // below every real key
     __syncthreads();
     uint64_t x[KPT];
 #pragma unroll
@@ -200,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
     __syncthreads();
 
     // 6. keep = count - 1; qo_indptr = exclusive scan of the counts (block scan)
-    constexpr int kPer = kMaxReqs / kThreads;  // 8 requests per thread
+    constexpr int kPer = (NT == kThreads ? kMaxReqs : kSmallMax) / NT;  // requests per thread: 8 or 2
     int loc[kPer];
     int rsum = 0;
     for (int e = 0; e < kPer; e++) {
@@ -228,7 +237,7 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
         }
         pos += loc[e];
     }
-    if (tid == kThreads - 1) {
+    if (tid == NT - 1) {
         qo_indptr[R] = pos;  // == K
         if (PREP) qs[R] = pos;
     }
@@ -239,14 +248,14 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
         int tk[KPT], Lc[KPT];
 #pragma unroll
         for (int e = 0; e < KPT; e++) {
-            const int p = tid + e * kThreads;
+            const int p = tid + e * NT;
             tk[e] = p < N ? pr.block_tokens[p] : 0;
             Lc[e] = p < N ? pr.ctx[p / b] : 0;
         }
         int* kvs = cnt;  // key counts for the plan (the counts are no longer needed)
 #pragma unroll
         for (int e = 0; e < KPT; e++) {
-            const int p = tid + e * kThreads;
+            const int p = tid + e * NT;
             if (p >= N) continue;
             const int i = p / b, j = p - i * b;
             const int q0 = qs[i], k_i = qs[i + 1] - q0;
@@ -264,8 +273,8 @@ __global__ __launch_bounds__(kThreads) void budget_kernel(BudgetArgs a, const fl
         if (!pr.plan) return;
         __syncthreads();
         // 8. the verify-attention work plan over those key counts
-        int* cursor = qs + ((R + 1 + 63) & ~63);
-        build_attn_plan<kThreads>(pr.pa, [&](int i, int& q0, int& k_i, int& kv) {
+        int* cursor = NT == kThreads ? qs + ((R + 1 + 63) & ~63) : cnt + kSmallMax;
+        build_attn_plan<NT>(pr.pa, [&](int i, int& q0, int& k_i, int& kv) {
             q0 = qs[i];
             k_i = qs[i + 1] - q0;
             kv = kvs[i];
@@ -301,15 +310,21 @@ hipError_t launch_budget_kernel(const sv_budget_desc& d, const float* conf, int3
                                 int32_t* sel, float* scores, uint64_t* utility, const PrepArgs& pr,
                                 hipStream_t stream) {
     const BudgetArgs a = budget_args(d);
-    const int64_t kpt = ((int64_t)d.num_reqs * d.block + kThreads - 1) / kThreads;
-#define SV_LAUNCH_BUDGET(KP) \
-    hipLaunchKernelGGL((budget_kernel<KP, PREP>), dim3(1), dim3(kThreads), 0, stream, a, conf, keep, qo_indptr, sel, \
+    const int64_t N = (int64_t)d.num_reqs * d.block;
+#define SV_LAUNCH_BUDGET(T, KP) \
+    hipLaunchKernelGGL((budget_kernel<T, KP, PREP>), dim3(1), dim3(T), 0, stream, a, conf, keep, qo_indptr, sel, \
                        scores, utility, pr)
-    if (kpt <= 1) SV_LAUNCH_BUDGET(1);
-    else if (kpt <= 2) SV_LAUNCH_BUDGET(2);
-    else if (kpt <= 4) SV_LAUNCH_BUDGET(4);
-    else if (kpt <= 8) SV_LAUNCH_BUDGET(8);
-    else SV_LAUNCH_BUDGET(16);
+    if (N <= kSmallMax) {  // (R <= N)
+        if (N <= kWave) SV_LAUNCH_BUDGET(kWave, 1);
+        else SV_LAUNCH_BUDGET(kWave, 2);
+    } else {
+        const int64_t kpt = (N + kThreads - 1) / kThreads;
+        if (kpt <= 1) SV_LAUNCH_BUDGET(kThreads, 1);
+        else if (kpt <= 2) SV_LAUNCH_BUDGET(kThreads, 2);
+        else if (kpt <= 4) SV_LAUNCH_BUDGET(kThreads, 4);
+        else if (kpt <= 8) SV_LAUNCH_BUDGET(kThreads, 8);
+        else SV_LAUNCH_BUDGET(kThreads, 16);
+    }
 #undef SV_LAUNCH_BUDGET
     return hipGetLastError();
 }
