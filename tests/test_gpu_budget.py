@@ -111,6 +111,21 @@ def test_random_budgets(dev, orc, seed, style):
         assert_same(g, o)
 
 
+@pytest.mark.parametrize("R,D", [(64, 0), (13, 4), (8, 15), (16, 7), (43, 2), (128, 0), (129, 0)])
+@pytest.mark.parametrize("style", ["ties", "dirty"])
+def test_one_wave_boundaries(dev, orc, R, D, style):
+    """Rounds at the edges of the one-wave form of the budget kernel (R*b of 64 and 65, of
+    128, and 129, the first that runs on 512 threads) with tied and dirty confidences: every
+    budget equals the oracle's bit for bit, in both modes."""
+    rng = np.random.default_rng(R * 97 + D)
+    conf = _conf(rng, R, D, style)
+    say("budget one-wave edge", R, D, style)
+    cost = np.array([20000, 21000, 23000, 26000], np.uint32)
+    assert_same(gpu_budget(dev, conf, "cost", cost=cost), orc.budget(conf, "cost", cost=cost))
+    for K in (R, (R * (D + 1) + R) // 2, R * (D + 1)):
+        assert_same(gpu_budget(dev, conf, "fixed", fixed=K), orc.budget(conf, "fixed", fixed_budget=K))
+
+
 @pytest.mark.parametrize("R,D", [(1, 0), (1, 15), (512, 15), (4096, 1), (2730, 2), (64, 15)])
 def test_size_limits(dev, orc, R, D):
     rng = np.random.default_rng(R * 31 + D)

@@ -99,11 +99,14 @@ def test_prepare_round_equals_separate_calls(dev, orc, name):
         assert torch.equal(rnd.attn_lse[:K], ref["attn_lse"][:K]), (name, "plan + run", layer)
 
 
-@pytest.mark.parametrize("R,b,total_cut", [(4096, 2, 0), (512, 16, 0), (64, 16, 37), (3, 1, 0)])
+@pytest.mark.parametrize("R,b,total_cut", [(4096, 2, 0), (512, 16, 0), (64, 16, 37), (3, 1, 0), (8, 16, 0),
+                                             (65, 1, 0), (43, 3, 5)])
 def test_prepare_round_budget_and_packing_edges(dev, orc, R, b, total_cut):
     """The largest budgets (4096 requests; 8192 positions), a packed batch with fewer rows
-    than the budget keeps (rows past total_max are dropped and kv_lens keeps L_i), and
-    blocks of one position: the fused set-up against the separate calls and the oracles."""
+    than the budget keeps (rows past total_max are dropped and kv_lens keeps L_i), blocks
+    of one position, and the edges of the one-wave form (128 positions; 65 positions of one
+    token; 129 positions on 512 threads): the fused set-up against the separate calls and
+    the oracles."""
     import torch
     from paper_2607_25852_amd import binding as B, synth
     from paper_2607_25852_amd.round import to_dev
