@@ -7,7 +7,8 @@ sv_spec_accept, with every output checked against the oracles:
 - acceptance under the logits-mode contract margins.
 The shapes vary what the named workloads hold fixed: GQA group 1-16 (whole-tile waves
 above 128 rows per kv-head group), head dim 64/128, pages of 1-128 tokens, contexts from
-0 to 2000 keys, vocabularies of 2-6000, bf16 and fp32, cost-table and fixed budgets.
+0 to 2000 keys, vocabularies of 2-6000, bf16 and fp32, cost-table and fixed budgets,
+and the temperature of acceptance (1, 0 = greedy verification, 0.6, 1.7).
 Unowned pages and slots hold NaN. Seeded; each case names its shape before its GPU step.
 """
 import numpy as np
@@ -48,14 +49,22 @@ def _draw(seed):
                              budget, 9000 + seed)
 
 
+TEMPERATURES = (1.0, 0.0, 0.6, 1.0, 1.7, 1.0)
+
+
 @pytest.mark.parametrize("seed", range(48))
 def test_random_round(dev, orc, seed):
     import torch
-    from paper_2607_25852_amd import synth
+    from paper_2607_25852_amd import binding as B, synth
     from paper_2607_25852_amd.round import DeviceRound
     cfg = _draw(seed)
-    say("random round", seed, cfg)
+    T = TEMPERATURES[seed % len(TEMPERATURES)]
+    say("random round", seed, cfg, "T", T)
     rnd = DeviceRound(cfg, kind="logits", fill_unused=float("nan"))
+    if T != 1.0:
+        rnd.xdesc = B.accept_desc(cfg.R, cfg.b, cfg.V, B.SV_LOGITS, B.SV_F32 if cfg.dtype == "f32" else B.SV_BF16,
+                                  temperature=T)
+        rnd.acc_ws = torch.empty(max(B.accept_workspace_size(rnd.xdesc), 256), dtype=torch.uint8, device="cuda")
     for name in ("keep", "qo", "kv_lens", "attn_out", "attn_lse", "accept_len", "out_tokens"):
         t = getattr(rnd, name)
         t.fill_(float("nan") if t.dtype.is_floating_point else -7)
@@ -90,11 +99,17 @@ def test_random_round(dev, orc, seed):
     ok, stats = compare_attention(out[rows, heads], lse[rows, heads], ref_o, ref_l, cfg.dtype)
     say("random round", seed, "attention", stats)
     assert ok, stats
-    # acceptance: the contract margins (probability rows of the logits, then the draw)
+    # acceptance: greedy verification bit for bit (argmax, no arithmetic); sampling under the
+    # contract margins (probability rows of the logits, then the draw)
     o = orc.accept(rnd.target_host, rnd.draft_host, rnd.lr["draft_tokens"], qo, rnd.ua_host, rnd.us_host,
-                   kind="logits", dtype=cfg.dtype, diagnostics=True)
+                   kind="logits", dtype=cfg.dtype, temperature=T, diagnostics=T != 0.0)
     g = dict(accept_len=rnd.accept_len.cpu().numpy(), out_tokens=rnd.out_tokens.cpu().numpy(),
              flags=rnd.flags.cpu().numpy())
+    if T == 0.0:
+        np.testing.assert_array_equal(g["accept_len"], o["accept_len"])
+        np.testing.assert_array_equal(g["out_tokens"], o["out_tokens"])
+        np.testing.assert_array_equal(g["flags"], o["flags"])
+        return
     exact, marginal, failures = classify_accept(g, o, rnd.ua_host)
     say("random round", seed, "acceptance exact", exact, "marginal", marginal)
     assert not failures, failures[:5]
