@@ -115,3 +115,29 @@ def test_random_round(dev, orc, seed):
     assert not failures, failures[:5]
     assert marginal <= 1
     assert np.all(g["accept_len"] <= np.diff(qo) - 1)
+
+
+@pytest.mark.parametrize("seed", range(100, 116))
+def test_random_round_probability_rows(dev, orc, seed):
+    """The same random rounds with fp32 probability rows: acceptance must equal the
+    oracle bit for bit (no rounding separates the two sides)."""
+    import torch
+    from paper_2607_25852_amd import synth
+    from paper_2607_25852_amd.round import DeviceRound
+    cfg = _draw(seed)
+    say("random round, probability rows", seed, cfg)
+    rnd = DeviceRound(cfg, kind="probs", fill_unused=float("nan"))
+    rnd.accept_len.fill_(-7)
+    rnd.out_tokens.fill_(-7)
+    rnd.run()
+    torch.cuda.synchronize()
+    conf = rnd.lr["conf"]
+    ob = (orc.budget(conf, "fixed", fixed_budget=cfg.budget[1]) if cfg.budget[0] == "fixed"
+          else orc.budget(conf, "cost", cost=synth.profiled_cost(cfg.R, cfg.b)))
+    qo = ob["qo_indptr"]
+    np.testing.assert_array_equal(rnd.qo.cpu().numpy(), qo)
+    o = orc.accept(rnd.target_host, rnd.draft_host, rnd.lr["draft_tokens"], qo, rnd.ua_host, rnd.us_host,
+                   kind="probs")
+    np.testing.assert_array_equal(rnd.accept_len.cpu().numpy(), o["accept_len"])
+    np.testing.assert_array_equal(rnd.out_tokens.cpu().numpy(), o["out_tokens"])
+    np.testing.assert_array_equal(rnd.flags.cpu().numpy(), o["flags"])
