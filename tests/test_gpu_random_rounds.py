@@ -141,3 +141,42 @@ def test_random_round_probability_rows(dev, orc, seed):
     np.testing.assert_array_equal(rnd.accept_len.cpu().numpy(), o["accept_len"])
     np.testing.assert_array_equal(rnd.out_tokens.cpu().numpy(), o["out_tokens"])
     np.testing.assert_array_equal(rnd.flags.cpu().numpy(), o["flags"])
+
+
+@pytest.mark.parametrize("seed", range(200, 216))
+def test_random_round_with_draft_statistics(dev, seed):
+    """The drafter's side of the random rounds: sv_draft_stats on the draft rows against
+    the oracle (m, S and the confidence), then sv_spec_accept_stats with those statistics
+    equal to sv_spec_accept on the same inputs, bit for bit, at T = 1, 0.6 and 1.7."""
+    import torch
+    from paper_2607_25852_amd import binding as B
+    from paper_2607_25852_amd.round import DeviceRound
+    from test_gpu_draft_stats import check_stats
+    cfg = _draw(seed)
+    T = (1.0, 0.6, 1.7, 1.0)[seed % 4]
+    say("random round, draft statistics", seed, cfg, "T", T)
+    rnd = DeviceRound(cfg, kind="logits", with_attn=False)
+    R, b, V = cfg.R, cfg.b, cfg.V
+    D = b - 1
+    dt = B.SV_F32 if cfg.dtype == "f32" else B.SV_BF16
+    dsd = B.draft_stats_desc(R, D, V, dt, T)
+    dws = torch.empty(max(B.draft_stats_workspace_size(dsd), 256), dtype=torch.uint8, device="cuda")
+    stats = torch.full((R * D, 2), float("nan"), dtype=torch.float32, device="cuda")
+    conf = torch.full((R * D,), float("nan"), dtype=torch.float32, device="cuda")
+    B.draft_stats(dsd, rnd.draft, stats, conf, dws)
+    xd = B.accept_desc(R, b, V, B.SV_LOGITS, dt, temperature=T)
+    aws = torch.empty(max(B.accept_workspace_size(xd), 256), dtype=torch.uint8, device="cuda")
+
+    def outs():
+        return (torch.full((R,), -9, dtype=torch.int32, device="cuda"),
+                torch.full((R, b), -9, dtype=torch.int32, device="cuda"),
+                torch.full((R,), -9, dtype=torch.int32, device="cuda"))
+    a1, o1, f1 = outs()
+    a2, o2, f2 = outs()
+    B.spec_accept(xd, rnd.target, rnd.draft, rnd.tokens, rnd.qo, rnd.u_accept, rnd.u_sample, a1, o1, f1, aws)
+    B.spec_accept_stats(xd, rnd.target, rnd.draft, stats, rnd.tokens, rnd.qo, rnd.u_accept, rnd.u_sample, a2, o2,
+                        f2, aws)
+    torch.cuda.synchronize()
+    check_stats(stats, conf, rnd.draft_host, cfg.dtype, T)
+    for x, y in ((a1, a2), (o1, o2), (f1, f2)):
+        assert torch.equal(x, y)
