@@ -137,6 +137,27 @@ def test_append_bit_exact(dev, R, b, Hkv, d, P, dtype, seed):
     assert (gk != kc).any() or int(qo[-1]) == 0  # something was written
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_append_random_shapes(dev, seed):
+    """Random shapes (requests, block, kv-heads, row lengths of 16-byte multiples up to
+    256 elements, pages of 1-512 tokens, bf16 and fp32), each with the malformed requests
+    of the fixed cases: the whole caches equal the oracle's, bit for bit."""
+    rng = np.random.default_rng(7000 + seed)
+    dtype = "f32" if seed % 3 == 0 else "bf16"
+    unit = 4 if dtype == "f32" else 8
+    R = int(rng.integers(1, 48))
+    b = int(rng.integers(1, 17))
+    Hkv = int(rng.integers(1, 9))
+    d = unit * int(rng.integers(1, 256 // unit + 1))
+    P = 1 << int(rng.integers(0, 10))
+    say(f"append random seed={seed} R={R} b={b} Hkv={Hkv} d={d} P={P} {dtype}")
+    k_new, v_new, pt, qo, L, kc, vc = _append_case(rng, R, b, Hkv, d, P, dtype, 2000)
+    gk, gv = gpu_append(dev, k_new, v_new, pt, qo, L, kc, vc, b, dtype)
+    wk, wv = oracle.append_kv(k_new, v_new, pt, qo, L, kc, vc, b)
+    np.testing.assert_array_equal(gk, wk)
+    np.testing.assert_array_equal(gv, wv)
+
+
 def test_append_full_c64_b16_shape(dev):
     """The c64_b16 launch shape (64 requests, block 16, 8 kv-heads, d 128, 64-token
     pages, bf16) with contexts up to 32768 tokens."""
